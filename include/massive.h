@@ -1,0 +1,166 @@
+/*
+ * massive.h - C ABI of libmassive: one graph partition's per-minibatch
+ * sampling + halo prefetch buffer + feature gather, after MassiveGNN
+ * (Sarkar, Ghosh, Tallent, Jannesari, arXiv 2410.22697), on one MI355X.
+ *
+ * The three calls follow the paper's procedures:
+ *   massive_init        INITIALIZE_PREFETCHER (Algorithm 1)
+ *   massive_sample      PREFETCH_WITH_EVICTION up to the eviction check
+ *                       (Algorithm 2: NeighborSampler, hit/miss split, S_E
+ *                       decay, local/buffer copies, miss fetch, S_A update)
+ *   massive_evict_step  the periodic round of Algorithm 2 (EVICT_AND_REPLACE
+ *                       with the score swap of Section IV-B, threshold Eq. 1)
+ *
+ * Ids. The partition's nodes carry partition-local ids: local (owned)
+ * nodes [0, L), halo (remote) nodes [L, L+H). The prefetcher's state and the
+ * eviction outputs use halo indices h = id - L in [0, H).
+ *
+ * Semantics (readings of the paper, fixed so that results are exact):
+ *   - The sampler walks G_p, the CSR of the subgraph induced on local + halo
+ *     nodes. Fanouts are hop-first. Hop k (1-based) samples for every node
+ *     of frontier F_{k-1}; new nodes are appended in ascending id, so F_k is
+ *     a prefix of F_{k+1} and the seeds come first.
+ *   - For a row v of length d at global step t, hop k: if d <= fanout every
+ *     position is kept; otherwise the fanout positions j with the smallest
+ *     (key_j, j), where key_j is word (j mod 4) of Philox4x32-10 (Salmon et
+ *     al., SC'11) with counter (j/4, v, t, k) and key (seed_lo, seed_hi).
+ *     Sampled neighbours are emitted in ascending j.
+ *   - Halo rank orders halo nodes by (degree desc, global id asc); the
+ *     buffer starts with the cap = floor(H * buffer_pct / 100) best ranked.
+ *   - Hits/misses use the buffer as it stood at the start of the step.
+ *     Every step: S_E *= gamma (fp32, one product per step) for each
+ *     buffered node not sampled; S_A += 1 for each miss.
+ *   - t counts steps across epochs from 0. After step t, if t > 0 and
+ *     t mod delta == 0, the round evicts the slots with S_E < alpha, where
+ *     alpha is gamma multiplied delta times in fp32, and replaces them with
+ *     the unbuffered halo nodes of highest (S_A, then rank); evicted slots
+ *     in ascending order are paired with replacements in that order. If
+ *     there are fewer candidates k' than evictions, the k' slots with the
+ *     smallest (S_E, rank) are evicted. Swap: evicted node's S_A := its last
+ *     S_E, slot's S_E := the replacement's last S_A, replacement's S_A := -1.
+ *
+ * Threading: calls on one context must not overlap. Different contexts are
+ * independent. Every call returns a status; nothing throws across the ABI.
+ */
+#ifndef MASSIVE_H
+#define MASSIVE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define MASSIVE_OK 0
+#define MASSIVE_EINVAL (-1)    /* bad argument (message in massive_last_error) */
+#define MASSIVE_ECAPACITY (-2) /* an output buffer is smaller than the bound  */
+#define MASSIVE_ENOMEM (-3)    /* device or host allocation failed            */
+#define MASSIVE_EHIP (-4)      /* HIP runtime error                           */
+#define MASSIVE_ESTATE (-5)    /* call out of order (see massive_sample)      */
+
+#define MASSIVE_MAX_HOPS 8
+
+typedef struct massive_ctx massive_ctx;
+
+/* Inputs of massive_init. Every host array is read during the call only,
+ * except halo_store, which the context borrows until massive_destroy. */
+typedef struct {
+  int32_t L;                  /* local nodes, ids [0, L)                      */
+  int32_t H;                  /* halo nodes, ids [L, L+H)                      */
+  const int64_t* indptr;      /* host [L+H+1], G_p row offsets (int64)        */
+  const int32_t* indices;     /* host [indptr[L+H]], partition-local ids      */
+  const int32_t* halo_gid;    /* host [H], global id of halo h (rank ties)    */
+  const int64_t* halo_degree; /* host [H], degree used to rank halo nodes     */
+  const void* local_feat;     /* host [L * row_bytes], copied into HBM        */
+  const void* halo_store;     /* PINNED host [H * row_bytes] (hipHostMalloc'd,
+                                 e.g. a torch pin_memory tensor): the remote
+                                 features; read by the GPU over the host link */
+  int64_t row_bytes;          /* bytes per feature row, multiple of 4         */
+  int32_t K;                  /* hops, 1..MASSIVE_MAX_HOPS                     */
+  int32_t fanout[MASSIVE_MAX_HOPS]; /* hop-first fanouts, each >= 1           */
+  int32_t buffer_pct;         /* f_p^h as an integer percent, 0..100          */
+  float gamma;                /* decay factor, 0 < gamma <= 1                 */
+  int32_t delta;              /* eviction interval, >= 1                      */
+  uint64_t seed;              /* Philox key                                   */
+  void* stream;               /* hipStream_t for all work (NULL: default)     */
+} massive_init_args;
+
+/* Creates a context: uploads G_p and local features to HBM, ranks the halo,
+ * fills the HBM buffer with the cap best-ranked halo rows from halo_store,
+ * and sets S_E = 1, S_A = -1 / 0. On failure *out is NULL and the message is
+ * in massive_last_error(NULL). */
+int massive_init(const massive_init_args* args, massive_ctx** out);
+
+/* Upper bounds on the output sizes of a batch of n_seeds seeds:
+ * n_bound[0..K] frontier sizes, e_bound[0..K-1] sampled edges per hop. */
+int massive_output_bounds(const massive_ctx* ctx, int32_t n_seeds, int64_t* n_bound,
+                          int64_t* e_bound);
+
+/* Caller-owned device buffers of one batch, plus the sizes written back.
+ * Capacities are in elements; each must be at least the bound above. */
+typedef struct {
+  int32_t* nodes;                          /* [nodes_cap] F_K; F_k = nodes[0:n[k]] */
+  uint8_t* mask;                           /* [nodes_cap] 0 local, 1 hit, 2 miss   */
+  void* feat;                              /* [nodes_cap * row_bytes], row i is the
+                                              feature row of nodes[i]             */
+  int64_t nodes_cap;
+  int32_t* indptr[MASSIVE_MAX_HOPS];       /* hop k: [n[k]+1] offsets into indices */
+  int32_t* indices[MASSIVE_MAX_HOPS];      /* hop k: [e[k]] positions in nodes     */
+  int64_t indptr_cap[MASSIVE_MAX_HOPS];
+  int64_t indices_cap[MASSIVE_MAX_HOPS];
+  /* written by massive_sample */
+  int64_t n[MASSIVE_MAX_HOPS + 1];         /* frontier sizes n_0..n_K              */
+  int64_t e[MASSIVE_MAX_HOPS];             /* sampled edges per hop                */
+  int64_t local, hits, misses;             /* input rows by class (unique nodes)   */
+} massive_batch;
+
+/* One minibatch at the context's current step t: samples K hops from the
+ * n_seeds device seeds (distinct local ids), classifies every frontier node
+ * against the buffer, updates the scores and gathers all feature rows (HBM
+ * rows from the local slab and the buffer, misses from halo_store). Returns
+ * after the batch is complete on the device; then t advances by one.
+ * MASSIVE_ESTATE if the previous step's massive_evict_step was not called.
+ * MASSIVE_EINVAL (no state change) if a seed is out of [0, L) or repeated. */
+int massive_sample(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
+
+/* The eviction round owed by the step just sampled; must be called once after
+ * every massive_sample. Runs the round iff that step t has t > 0 and
+ * t mod delta == 0, else sets *k_out = 0. Optional device outputs, each with
+ * room for cap entries: evicted halo ids, the slots they held (ascending),
+ * and their replacements. The replacement rows are copied from halo_store on
+ * a side stream that overlaps the next step's sampling; the next step's
+ * gather waits for them. */
+int massive_evict_step(massive_ctx* ctx, int32_t* evicted, int32_t* slots, int32_t* replaced,
+                       int64_t* k_out);
+
+/* Host copies of the prefetcher state (each pointer may be NULL):
+ * slot_id[cap] halo id per slot, S_E[cap], S_A[H], steps sampled so far. */
+int massive_get_state(massive_ctx* ctx, int32_t* slot_id, float* S_E, float* S_A, int64_t* t);
+
+/* Host copy of the HBM buffer's rows, [cap * row_bytes]. */
+int massive_get_buffer_rows(massive_ctx* ctx, void* host_out);
+
+/* cap (buffer slots), alpha, and the library's internal HIP streams. */
+int massive_info(const massive_ctx* ctx, int64_t* cap, float* alpha);
+
+/* Per-kernel-group timing with HIP events recorded on the stream each group
+ * runs on. enable != 0 turns it on (and clears the totals). */
+int massive_set_timing(massive_ctx* ctx, int enable);
+/* Totals since enabled: out_ms[i] summed milliseconds and out_calls[i]
+ * launches for i = 0 sample+dedup, 1 classify, 2 gather_hbm, 3 gather_miss,
+ * 4 eviction round, 5 refill. Synchronises the context's streams. */
+int massive_get_timing(massive_ctx* ctx, double* out_ms, int64_t* out_calls);
+
+/* Frees every device and host resource of the context. */
+int massive_destroy(massive_ctx* ctx);
+
+/* Message of the last failure on this context (ctx == NULL: of the last
+ * failed massive_init on this thread). Never NULL. */
+const char* massive_last_error(const massive_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MASSIVE_H */

@@ -74,6 +74,8 @@ def _load():
         lib.oracle_block_indices.restype = vp
         lib.oracle_get_state.argtypes = [vp, vp, vp, vp]
         lib.oracle_phase_times.argtypes = [vp, vp]
+        lib.oracle_sample_row.argtypes = [vp, vp, i32, i64, i32, i32, ctypes.c_uint64, vp]
+        lib.oracle_sample_row.restype = i64
         _lib = lib
     return _lib
 
@@ -84,6 +86,20 @@ def philox4x32_10(ctr: Sequence[int], key: Sequence[int]) -> List[int]:
     o = (ctypes.c_uint32 * 4)()
     _load().oracle_philox4x32_10(c, k, o)
     return list(o)
+
+
+def sample_row(indptr: np.ndarray, indices: np.ndarray, v: int, t: int, k: int, fanout: int,
+               seed: int = 0) -> np.ndarray:
+    """Neighbour ids the sampler chooses for node v at step t, hop k (1-based)."""
+    ip = np.ascontiguousarray(indptr, np.int64)
+    ix = np.ascontiguousarray(indices, np.int32)
+    d = int(ip[v + 1] - ip[v])
+    out = np.zeros(max(min(d, fanout), 1), np.int32)
+    m = _load().oracle_sample_row(ip.ctypes.data, ix.ctypes.data, int(v), int(t), int(k), int(fanout),
+                                  int(seed), out.ctypes.data)
+    if m < 0:
+        raise MemoryError("oracle_sample_row")
+    return out[:m]
 
 
 def _arr(ptr, dtype, n):

@@ -485,6 +485,27 @@ int oracle_evict_step(oracle_ctx* c, int32_t* evicted, int32_t* slots, int32_t* 
   return OR_OK;
 }
 
+/* The sampler's choice for one row, outside any context: the neighbour ids
+ * chosen for node v at step t, hop k (1-based), written to out (room for
+ * min(d, fanout)). Returns how many. Used to check single rows of large
+ * runs. */
+int64_t oracle_sample_row(const int64_t* indptr, const int32_t* indices, int32_t v, int64_t t, int32_t k,
+                          int32_t fanout, uint64_t seed, int32_t* out) {
+  oracle_ctx c;
+  memset(&c, 0, sizeof c);
+  c.a.seed = seed;
+  c.t = t;
+  int64_t start = indptr[v], d = indptr[v + 1] - start;
+  int64_t* sel = (int64_t*)malloc(sizeof(int64_t) * (size_t)(d + 1));
+  uint64_t* keybuf = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)(d + 1));
+  if (!sel || !keybuf) { free(sel); free(keybuf); return -1; }
+  int64_t m = choose_positions(&c, v, d, fanout, k, sel, keybuf);
+  for (int64_t q = 0; q < m; q++) out[q] = indices[start + sel[q]];
+  free(sel);
+  free(keybuf);
+  return m;
+}
+
 /* ---------------------------------------------------------------- access */
 int64_t oracle_cap(const oracle_ctx* c) { return c->cap; }
 float oracle_alpha(const oracle_ctx* c) { return c->alpha; }

@@ -1,0 +1,642 @@
+// buffer_kernels.hpp - halo prefetch buffer: lookup, scoring, gather,
+// eviction select, replacement select, swap (Algorithm 2 and Section IV-B).
+#pragma once
+
+#include "common.hpp"
+#include "sample_kernels.hpp"
+
+namespace ms {
+
+constexpr uint64_t kEmpty = ~0ull;
+
+// MurmurHash3 fmix32 finaliser (public domain).
+__device__ __forceinline__ uint32_t fmix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x85ebca6bu;
+  x ^= x >> 13;
+  x *= 0xc2b2ae35u;
+  x ^= x >> 16;
+  return x;
+}
+
+// Open-addressing table (linear probing, load <= 1/2): entry = slot << 32 | h.
+__device__ __forceinline__ int32_t hash_find(const uint64_t* __restrict__ tab, uint32_t mask, int32_t h) {
+  uint32_t i = fmix32((uint32_t)h) & mask;
+  while (true) {
+    const uint64_t e = tab[i];
+    if ((uint32_t)e == (uint32_t)h) return (int32_t)(e >> 32);
+    if (e == kEmpty) return -1;
+    i = (i + 1) & mask;
+  }
+}
+
+__global__ void k_hash_insert(uint64_t* __restrict__ tab, uint32_t mask, const int32_t* __restrict__ slot_id,
+                              int64_t cap) {
+  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < cap;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t h = slot_id[s];
+    const uint64_t entry = ((uint64_t)(uint32_t)s << 32) | (uint32_t)h;
+    uint32_t i = fmix32((uint32_t)h) & mask;
+    while (atomicCAS((unsigned long long*)&tab[i], (unsigned long long)kEmpty, (unsigned long long)entry) !=
+           (unsigned long long)kEmpty)
+      i = (i + 1) & mask;
+  }
+}
+
+template <typename T>
+__global__ void k_fill(T* __restrict__ p, int64_t n, T v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// ------------------------------------------------------------- classify
+// For every frontier node: local / buffer hit / miss against the buffer as it
+// stands at the start of the step. Hits count this step for the lazy S_E
+// decay (hitcnt); misses take S_A += 1. Rows go to two gather lists, (row,
+// HBM slab row) and (row, halo id), compacted with wave ballots and one
+// atomic per wave. Also clears pos_of for the next step.
+struct ClassifyArgs {
+  const int32_t* nodes;
+  StepSizes* sz;
+  int32_t K;
+  int32_t L;
+  const uint64_t* tab;
+  uint32_t tmask;
+  int32_t* hitcnt;
+  float* S_A;
+  int32_t* pos_of;
+  uint8_t* mask;
+  int2* hbm_list;
+  int2* miss_list;
+};
+
+constexpr int kClsNT = 256;
+constexpr int kClsItems = 8;  // rows per thread: one block classifies 2048 rows
+
+// Block-level aggregation: each block counts its rows per class, takes one
+// base per list with a single atomic, and places rows with wave ballots.
+__global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
+  constexpr int NW = kClsNT / MS_WAVE;
+  __shared__ int32_t wc[NW][3];          // per-wave counts: hbm, miss, local
+  __shared__ unsigned long long base[2];
+  if (a.sz->status) return;
+  const int64_t n = a.sz->n[a.K];
+  const int lane = lane_id(), wave = wave_id();
+  const int64_t tile = (int64_t)kClsNT * kClsItems;
+  for (int64_t b0 = (int64_t)blockIdx.x * tile; b0 < n; b0 += (int64_t)gridDim.x * tile) {
+    int cls[kClsItems];
+    int32_t src[kClsItems];
+    int ch = 0, cm = 0, cl = 0;
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) {
+      // wave w of item it covers rows b0 + it*256 + w*64 + lane
+      const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
+      cls[it] = -1;
+      src[it] = 0;
+      if (i < n) {
+        const int32_t v = a.nodes[i];
+        a.pos_of[v] = -1;
+        if (v < a.L) {
+          cls[it] = 0;
+          src[it] = v;
+        } else {
+          const int32_t h = v - a.L;
+          const int32_t slot = hash_find(a.tab, a.tmask, h);
+          if (slot >= 0) {
+            cls[it] = 1;
+            src[it] = a.L + slot;
+            a.hitcnt[slot] += 1;
+          } else {
+            cls[it] = 2;
+            src[it] = h;
+            atomicAdd(&a.S_A[h], 1.0f);
+          }
+        }
+        a.mask[i] = (uint8_t)cls[it];
+      }
+      ch += __popcll(ballot(cls[it] == 0 || cls[it] == 1));
+      cm += __popcll(ballot(cls[it] == 2));
+      cl += __popcll(ballot(cls[it] == 0));
+    }
+    if (lane == 0) {
+      wc[wave][0] = ch;
+      wc[wave][1] = cm;
+      wc[wave][2] = cl;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int th = 0, tm = 0, tl = 0;
+      for (int w = 0; w < NW; ++w) {
+        th += wc[w][0];
+        tm += wc[w][1];
+        tl += wc[w][2];
+      }
+      base[0] = th ? atomicAdd((unsigned long long*)&a.sz->n_hbm, (unsigned long long)th) : 0ull;
+      base[1] = tm ? atomicAdd((unsigned long long*)&a.sz->n_miss, (unsigned long long)tm) : 0ull;
+      if (tl) atomicAdd((unsigned long long*)&a.sz->local, (unsigned long long)tl);
+      if (th - tl) atomicAdd((unsigned long long*)&a.sz->hits, (unsigned long long)(th - tl));
+      if (tm) atomicAdd((unsigned long long*)&a.sz->misses, (unsigned long long)tm);
+    }
+    __syncthreads();
+    // this wave's offset inside the block's share of each list
+    unsigned long long oh = base[0], om = base[1];
+    for (int w = 0; w < wave; ++w) {
+      oh += wc[w][0];
+      om += wc[w][1];
+    }
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) {
+      const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
+      const uint64_t mh = ballot(cls[it] == 0 || cls[it] == 1);
+      const uint64_t mm = ballot(cls[it] == 2);
+      if (cls[it] == 0 || cls[it] == 1) a.hbm_list[oh + lanes_below(mh)] = make_int2((int32_t)i, src[it]);
+      else if (cls[it] == 2) a.miss_list[om + lanes_below(mm)] = make_int2((int32_t)i, src[it]);
+      oh += __popcll(mh);
+      om += __popcll(mm);
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- gather
+// dst row list[x].x <- src row list[x].y, as a bit copy of row_bytes. The
+// (row, chunk) work is flattened so every lane moves one vector per chunk
+// whatever the row size; four chunks are in flight per lane.
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+
+template <typename V>
+__device__ __forceinline__ void gather_body(const int2* __restrict__ list, const int64_t* __restrict__ count,
+                                            const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, int64_t rb,
+                                            uint32_t cpr, uint64_t magic) {
+  const uint64_t n = (uint64_t)*count;
+  const uint64_t total = n * cpr;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  auto split = [&](uint64_t cc, uint64_t& task, uint32_t& ch) {
+    task = cpr == 1 ? cc : __umul64hi(cc, magic);
+    ch = (uint32_t)(cc - task * cpr);
+  };
+  for (; c + 3 * stride < total; c += 4 * stride) {
+    V v[4];
+    int2 e[4];
+    uint32_t ch[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint64_t task;
+      split(c + u * stride, task, ch[u]);
+      e[u] = list[task];
+      v[u] = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e[u].y * rb + (uint64_t)ch[u] * sizeof(V));
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e[u].x * rb +
+                                                             (uint64_t)ch[u] * sizeof(V)));
+  }
+  for (; c < total; c += stride) {
+    uint64_t task;
+    uint32_t ch;
+    split(c, task, ch);
+    const int2 e = list[task];
+    const V v = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e.y * rb + (uint64_t)ch * sizeof(V));
+    __builtin_nontemporal_store(v, reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e.x * rb + (uint64_t)ch * sizeof(V)));
+  }
+}
+
+// local rows and buffer hits: HBM slab -> output rows
+template <typename V>
+__global__ __launch_bounds__(256) void k_gather_hbm(const int2* __restrict__ list, const int64_t* __restrict__ count,
+                                                    const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                    int64_t rb, uint32_t cpr, uint64_t magic) {
+  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+}
+// misses: pinned host store (over the host link) -> output rows
+template <typename V>
+__global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int64_t* __restrict__ count,
+                                                     const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                     int64_t rb, uint32_t cpr, uint64_t magic) {
+  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+}
+// eviction refill: pinned host store -> buffer slots
+template <typename V>
+__global__ __launch_bounds__(256) void k_refill(const int2* __restrict__ list, const int64_t* __restrict__ count,
+                                                const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                int64_t rb, uint32_t cpr, uint64_t magic) {
+  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+}
+
+// ------------------------------------------------------------ lazy decay
+// S_E[s] is multiplied by gamma once for every step in which slot s was not
+// hit since the last materialisation: `steps` steps elapsed, hitcnt[s] of
+// them hits. Same fp32 product sequence as one multiply per step.
+__global__ void k_materialize(float* __restrict__ S_E, int32_t* __restrict__ hitcnt, int64_t cap, int32_t steps,
+                              float gamma) {
+  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < cap; s += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t u = steps - hitcnt[s];
+    float x = S_E[s];
+    for (int32_t j = 0; j < u; ++j) x = __fmul_rn(x, gamma);
+    S_E[s] = x;
+    hitcnt[s] = 0;
+  }
+}
+
+// ------------------------------------------------- ordered flag compaction
+// E = [s : S_E[s] < alpha] in ascending s, as count / scan / emit.
+__global__ __launch_bounds__(kScanNT) void k_evict_count(const float* __restrict__ S_E, int64_t cap, float alpha,
+                                                         int32_t* __restrict__ partials) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  int32_t s = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
+    s += (i < cap && S_E[i] < alpha) ? 1 : 0;
+  }
+  s = block_sum<kScanNT>(s, lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(kScanNT) void k_evict_emit(const float* __restrict__ S_E, int64_t cap, float alpha,
+                                                        const int32_t* __restrict__ partials,
+                                                        int32_t* __restrict__ E) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  bool f[kScanItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t i = base + it;
+    f[it] = i < cap && S_E[i] < alpha;
+    s += f[it];
+  }
+  int32_t tot;
+  int32_t o = block_exclusive_scan<kScanNT>(s, lds, &tot) + partials[blockIdx.x];
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it)
+    if (f[it]) E[o++] = (int32_t)(base + it);
+}
+
+// |C| = number of unbuffered halo nodes (S_A >= 0).
+__global__ __launch_bounds__(256) void k_count_candidates(const float* __restrict__ S_A, int64_t H,
+                                                          int64_t* __restrict__ out) {
+  __shared__ int64_t lds[256 / MS_WAVE + 1];
+  int64_t c = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x)
+    c += S_A[i] >= 0.0f;
+  c = block_sum<256>(c, lds);
+  if (threadIdx.x == 0 && c) atomicAdd((unsigned long long*)out, (unsigned long long)c);
+}
+
+// ------------------------------------------------------ replacement select
+// Candidate key: bitwise NOT of the fp32 bits of S_A >= 0, so ascending key
+// is descending S_A. Radix select, 8 bits per pass from the top, finds the
+// key T of the k'-th candidate and how many candidates with key T to take.
+__device__ __forceinline__ uint32_t cand_key(float a) { return ~__float_as_uint(a); }
+
+__global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S_A, int64_t H,
+                                                     const RoundState* __restrict__ rs, int shift,
+                                                     uint32_t* __restrict__ ghist) {
+  __shared__ uint32_t hist[256];
+  hist[threadIdx.x] = 0;
+  __syncthreads();
+  const uint32_t prefix = rs->prefix, pmask = rs->pmask;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x) {
+    const float a = S_A[i];
+    if (a >= 0.0f) {
+      const uint32_t k = cand_key(a);
+      if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    }
+  }
+  __syncthreads();
+  if (hist[threadIdx.x]) atomicAdd(&ghist[threadIdx.x], hist[threadIdx.x]);
+}
+
+__global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs, uint32_t* __restrict__ ghist,
+                                                     int shift) {
+  __shared__ int64_t lds[256 / MS_WAVE + 1];
+  __shared__ int32_t pick;
+  __shared__ int64_t before;
+  if (threadIdx.x == 0) {
+    pick = -1;
+    before = 0;
+  }
+  __syncthreads();
+  const int64_t need = rs->need;
+  const int64_t c = ghist[threadIdx.x];
+  int64_t tot;
+  const int64_t ex = block_exclusive_scan<256>(c, lds, &tot);
+  if (ex < need && ex + c >= need) {
+    pick = threadIdx.x;
+    before = ex;
+  }
+  __syncthreads();
+  ghist[threadIdx.x] = 0;
+  if (threadIdx.x == 0) {
+    if (pick < 0) {  // fewer candidates than asked for: never expected
+      rs->bad |= 2;
+      rs->need = 0;
+    } else {
+      rs->need = need - before;
+      rs->prefix |= (uint32_t)pick << shift;
+      rs->pmask |= 255u << shift;
+    }
+  }
+}
+
+// In rank order r: candidates with key < T go to (keys, vals) for sorting,
+// the first `need` with key == T go straight to R[n_lt + ...].
+__global__ __launch_bounds__(kScanNT) void k_rank_count(const float* __restrict__ S_A,
+                                                        const int32_t* __restrict__ h_of_rank, int64_t H,
+                                                        const RoundState* __restrict__ rs,
+                                                        int32_t* __restrict__ p_lt, int32_t* __restrict__ p_eq) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const uint32_t T = rs->prefix;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  int32_t clt = 0, ceq = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t r = base + (int64_t)it * kScanNT + threadIdx.x;
+    if (r < H) {
+      const float a = S_A[h_of_rank[r]];
+      if (a >= 0.0f) {
+        const uint32_t k = cand_key(a);
+        clt += k < T;
+        ceq += k == T;
+      }
+    }
+  }
+  clt = block_sum<kScanNT>(clt, lds);
+  ceq = block_sum<kScanNT>(ceq, lds);
+  if (threadIdx.x == 0) {
+    p_lt[blockIdx.x] = clt;
+    p_eq[blockIdx.x] = ceq;
+  }
+}
+
+__global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__ S_A,
+                                                       const int32_t* __restrict__ h_of_rank, int64_t H,
+                                                       const RoundState* __restrict__ rs,
+                                                       const int32_t* __restrict__ p_lt,
+                                                       const int32_t* __restrict__ p_eq,
+                                                       uint32_t* __restrict__ keys, int32_t* __restrict__ vals,
+                                                       int32_t* __restrict__ R) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const uint32_t T = rs->prefix;
+  const int64_t need = rs->need, n_lt = rs->k - rs->need;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  uint32_t k[kScanItems];
+  int32_t h[kScanItems];
+  bool lt[kScanItems], eq[kScanItems];
+  int32_t clt = 0, ceq = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t r = base + it;
+    lt[it] = eq[it] = false;
+    if (r < H) {
+      h[it] = h_of_rank[r];
+      const float a = S_A[h[it]];
+      if (a >= 0.0f) {
+        k[it] = cand_key(a);
+        lt[it] = k[it] < T;
+        eq[it] = k[it] == T;
+      }
+    }
+    clt += lt[it];
+    ceq += eq[it];
+  }
+  int32_t tlt, teq;
+  int64_t olt = (int64_t)block_exclusive_scan<kScanNT>(clt, lds, &tlt) + p_lt[blockIdx.x];
+  int64_t oeq = (int64_t)block_exclusive_scan<kScanNT>(ceq, lds, &teq) + p_eq[blockIdx.x];
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    if (lt[it]) {
+      keys[olt] = k[it];
+      vals[olt] = h[it];
+      ++olt;
+    } else if (eq[it]) {
+      if (oeq < need) R[n_lt + oeq] = h[it];
+      ++oeq;
+    }
+  }
+}
+
+// ------------------------------------------------------ stable radix sort
+// LSD, 8 bits per pass, 2048 keys per block (256 threads x 8, striped so the
+// stable order within a block is (item, wave, lane)). Digit-major block
+// histograms are scanned into global offsets; ranks inside a block come from
+// wave match masks (8 ballots) and per-wave digit counters in LDS.
+constexpr int kSortNT = 256;
+constexpr int kSortItems = 8;
+constexpr int kSortTile = kSortNT * kSortItems;
+
+__global__ __launch_bounds__(kSortNT) void k_sort_hist(const uint32_t* __restrict__ keys, const int64_t* __restrict__ n_ptr,
+                                                       int64_t n_const, int64_t bound, int shift, int64_t nb,
+                                                       int32_t* __restrict__ hist) {
+  __shared__ int32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t n = min(size_of(n_ptr, n_const), bound);
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+#pragma unroll
+  for (int it = 0; it < kSortItems; ++it) {
+    const int64_t i = base + (int64_t)it * kSortNT + threadIdx.x;
+    if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nb + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ __launch_bounds__(kSortNT) void k_sort_scatter(const uint32_t* __restrict__ keys_in,
+                                                          const int32_t* __restrict__ vals_in,
+                                                          const int64_t* __restrict__ n_ptr, int64_t n_const,
+                                                          int64_t bound, int shift, int64_t nb,
+                                                          const int32_t* __restrict__ offs,
+                                                          uint32_t* __restrict__ keys_out,
+                                                          int32_t* __restrict__ vals_out) {
+  constexpr int NW = kSortNT / MS_WAVE;
+  __shared__ int32_t wcnt[NW][256];
+  __shared__ int32_t running[256];
+  __shared__ int32_t gbase[256];
+  const int lane = lane_id(), wave = wave_id();
+  for (int w = 0; w < NW; ++w) wcnt[w][threadIdx.x] = 0;
+  running[threadIdx.x] = 0;
+  gbase[threadIdx.x] = offs[(int64_t)threadIdx.x * nb + blockIdx.x];
+  __syncthreads();
+  const int64_t n = min(size_of(n_ptr, n_const), bound);
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  for (int it = 0; it < kSortItems; ++it) {
+    const int64_t i = base + (int64_t)it * kSortNT + threadIdx.x;
+    const bool valid = i < n;
+    const uint32_t k = valid ? keys_in[i] : 0u;
+    const int32_t val = valid ? vals_in[i] : 0;
+    const uint32_t dgt = (k >> shift) & 255u;
+    uint64_t peers = ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const uint64_t m = ballot((dgt >> b) & 1u);
+      peers &= ((dgt >> b) & 1u) ? m : ~m;
+    }
+    const int below = lanes_below(peers);
+    const bool leader = valid && ((peers >> lane) >> 1) == 0ull;  // highest lane of its digit
+    if (leader) wcnt[wave][dgt] = below + 1;
+    __syncthreads();
+    if (valid) {
+      int32_t r = running[dgt] + below;
+      for (int w = 0; w < wave; ++w) r += wcnt[w][dgt];
+      const int64_t dst = (int64_t)gbase[dgt] + r;
+      keys_out[dst] = k;
+      vals_out[dst] = val;
+    }
+    __syncthreads();
+    {
+      int32_t add = 0;
+      for (int w = 0; w < NW; ++w) {
+        add += wcnt[w][threadIdx.x];
+        wcnt[w][threadIdx.x] = 0;
+      }
+      running[threadIdx.x] += add;
+    }
+    __syncthreads();
+  }
+}
+
+// Generic exclusive scan of an int32 array with host-known length.
+__global__ __launch_bounds__(kScanNT) void k_tile_reduce(const int32_t* __restrict__ a, int64_t len,
+                                                         int32_t* __restrict__ partials) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  int32_t s = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
+    if (i < len) s += a[i];
+  }
+  s = block_sum<kScanNT>(s, lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(kScanNT) void k_tile_scan(int32_t* __restrict__ a, int64_t len,
+                                                       const int32_t* __restrict__ partials) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    v[it] = base + it < len ? a[base + it] : 0;
+    s += v[it];
+  }
+  int32_t tot;
+  int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot) + partials[blockIdx.x];
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    if (base + it < len) a[base + it] = ex;
+    ex += v[it];
+  }
+}
+
+// ---------------------------------------------------------- key builders
+// rank keys: low word = global id, high word = ~degree (degree desc).
+__global__ void k_rank_keys_lo(const int32_t* __restrict__ gid, int64_t H, uint32_t* __restrict__ keys,
+                               int32_t* __restrict__ vals) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x) {
+    keys[i] = (uint32_t)gid[i] ^ 0x80000000u;  // signed order as unsigned
+    vals[i] = (int32_t)i;
+  }
+}
+__global__ void k_rank_keys_hi(const int64_t* __restrict__ deg, const int32_t* __restrict__ vals, int64_t H,
+                               uint32_t* __restrict__ keys) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x) {
+    int64_t d = deg[vals[i]];
+    if (d < 0) d = 0;
+    if (d > 0xFFFFFFFFll) d = 0xFFFFFFFFll;
+    keys[i] = ~(uint32_t)d;
+  }
+}
+__global__ void k_rank_finish(const int32_t* __restrict__ h_of_rank, int64_t H, int32_t* __restrict__ rank_of) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < H; r += (int64_t)gridDim.x * blockDim.x)
+    rank_of[h_of_rank[r]] = (int32_t)r;
+}
+
+// Initial buffer: slot s holds the halo node of rank s.
+__global__ void k_init_buffer(const int32_t* __restrict__ h_of_rank, int64_t cap, int32_t L,
+                              int32_t* __restrict__ slot_id, float* __restrict__ S_E, int32_t* __restrict__ hitcnt,
+                              float* __restrict__ S_A, int2* __restrict__ fill) {
+  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < cap; s += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t h = h_of_rank[s];
+    slot_id[s] = h;
+    S_E[s] = 1.0f;
+    hitcnt[s] = 0;
+    S_A[h] = -1.0f;
+    fill[s] = make_int2((int32_t)(L + s), h);
+  }
+}
+
+// E-selection keys (only when fewer candidates than evictions):
+// low = rank of the slot's node, high = fp32 bits of S_E (S_E >= 0).
+__global__ void k_esel_keys_lo(const int32_t* __restrict__ E, const int64_t* __restrict__ n_ptr,
+                               const int32_t* __restrict__ slot_id, const int32_t* __restrict__ rank_of,
+                               uint32_t* __restrict__ keys, int32_t* __restrict__ vals) {
+  const int64_t n = *n_ptr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    keys[i] = (uint32_t)rank_of[slot_id[E[i]]];
+    vals[i] = E[i];
+  }
+}
+__global__ void k_esel_keys_hi(const int32_t* __restrict__ vals, const int64_t* __restrict__ n_ptr,
+                               const float* __restrict__ S_E, uint32_t* __restrict__ keys) {
+  const int64_t n = *n_ptr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    keys[i] = __float_as_uint(S_E[vals[i]]);
+}
+__global__ void k_esel_keys_slot(const int32_t* __restrict__ vals, const int64_t* __restrict__ n_ptr,
+                                 uint32_t* __restrict__ keys) {
+  const int64_t n = *n_ptr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    keys[i] = (uint32_t)vals[i];
+}
+
+// ------------------------------------------------------------------ swap
+// Pair E[i] (ascending slot) with R[i]; every read sees pre-round values
+// because the slots, the evicted nodes and the replacements are all
+// distinct, so no two threads touch the same entry.
+__global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict__ R, const int64_t* __restrict__ k_ptr,
+                       int32_t L, int64_t cap, int32_t H, int32_t* __restrict__ slot_id, float* __restrict__ S_E,
+                       float* __restrict__ S_A, int32_t* __restrict__ out_ev, int32_t* __restrict__ out_slot,
+                       int32_t* __restrict__ out_rep, int2* __restrict__ fill, int32_t* __restrict__ bad) {
+  const int64_t k = *k_ptr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < k; i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t s = E[i], r = R[i];
+    if (s < 0 || s >= cap || r < 0 || r >= H) {  // never expected: flag, do not touch memory
+      atomicOr(bad, 1);
+      fill[i] = make_int2(-1, -1);
+      continue;
+    }
+    const int32_t e = slot_id[s];
+    const float se = S_E[s], sa = S_A[r];
+    S_A[e] = se;
+    S_E[s] = sa;
+    S_A[r] = -1.0f;
+    slot_id[s] = r;
+    if (out_ev) out_ev[i] = e;
+    if (out_slot) out_slot[i] = s;
+    if (out_rep) out_rep[i] = r;
+    fill[i] = make_int2((int32_t)(L + s), r);
+  }
+}
+
+}  // namespace ms
+
+namespace ms {
+// G_p sanity: non-decreasing offsets, column ids inside [0, R).
+__global__ void k_validate_csr(const int64_t* __restrict__ indptr, int64_t R, const int32_t* __restrict__ indices,
+                               int64_t nnz, int32_t* __restrict__ bad) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R; i += stride)
+    if (indptr[i + 1] < indptr[i]) atomicOr(bad, 1);
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nnz; e += stride) {
+    const int32_t v = indices[e];
+    if (v < 0 || v >= R) atomicOr(bad, 2);
+  }
+}
+}  // namespace ms

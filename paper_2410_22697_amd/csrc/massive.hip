@@ -1,0 +1,729 @@
+// massive.hip - libmassive: the C ABI of include/massive.h on one MI355X.
+//
+// Streams: every step runs on the caller's stream ("main"); misses are
+// gathered from pinned host memory on a side stream concurrently with the
+// HBM gather; the refill copy of an eviction round runs on a copy stream and
+// overlaps the next step's sampling (the next HBM gather waits for it).
+// All device memory is allocated in massive_init; the per-step calls do not
+// allocate.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/massive.h"
+#include "buffer_kernels.hpp"
+#include "common.hpp"
+#include "sample_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_init_error;
+
+struct TimedRange {
+  hipEvent_t a, b;
+  int group;
+};
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
+  int64_t g = cdiv(std::max<int64_t>(n, 1), nt);
+  return (unsigned)std::min<int64_t>(std::max<int64_t>(g, 1), cap);
+}
+
+}  // namespace
+
+struct massive_ctx {
+  // configuration
+  int32_t L = 0, H = 0;
+  int64_t R = 0, nnz = 0, rb = 0;
+  int32_t K = 0;
+  int32_t fo[MASSIVE_MAX_HOPS] = {};
+  int32_t pct = 0;
+  float gamma = 1.0f;
+  int32_t delta = 1;
+  uint64_t seed = 0;
+  int64_t cap = 0, hcap = 0;
+  uint32_t hmask = 0;
+  float alpha = 1.0f;
+  int64_t W = 0;        // bitmap words
+  int64_t pmax = 0;     // partials capacity
+  int64_t sort_cap = 0; // radix sort capacity
+  int64_t host_blocks = 16;  // grid of the host-link gathers
+  // streams and events
+  hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
+  hipEvent_t ev_classified = nullptr, ev_miss_done = nullptr, ev_swap_done = nullptr, ev_refill_done = nullptr;
+  bool refill_pending = false;
+  // device memory
+  int64_t* d_indptr = nullptr;
+  int32_t* d_indices = nullptr;
+  uint8_t* d_slab = nullptr;          // [(L + cap) * rb]: local rows, then buffer rows
+  const uint8_t* d_store = nullptr;   // device view of the pinned halo store
+  int32_t* d_slot_id = nullptr;
+  float* d_S_E = nullptr;
+  int32_t* d_hitcnt = nullptr;
+  float* d_S_A = nullptr;
+  int32_t* d_rank_of = nullptr;
+  int32_t* d_h_of_rank = nullptr;
+  uint64_t* d_tab = nullptr;
+  int32_t* d_pos_of = nullptr;
+  uint32_t* d_bits = nullptr;
+  ms::StepSizes* d_sz = nullptr;
+  ms::StepSizes* h_sz = nullptr;      // pinned mailbox
+  ms::RoundState* d_rs = nullptr;
+  ms::RoundState* h_rs = nullptr;     // pinned mailbox
+  int32_t* d_part = nullptr;
+  int32_t* d_part2 = nullptr;
+  int2* d_hbm_list = nullptr;
+  int2* d_miss_list = nullptr;
+  int32_t* d_E = nullptr;
+  int32_t* d_R = nullptr;
+  int2* d_fill = nullptr;
+  uint32_t* d_k0 = nullptr;
+  uint32_t* d_k1 = nullptr;
+  int32_t* d_v0 = nullptr;
+  int32_t* d_v1 = nullptr;
+  int32_t* d_hist = nullptr;
+  uint32_t* d_ghist = nullptr;
+  // host-side step state
+  int64_t t = 0;        // steps sampled
+  int64_t mat_t = 0;    // S_E materialised through this many steps
+  bool pending_round = false;
+  bool broken = false;
+  // timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<TimedRange> pending;
+  double tms[6] = {};
+  int64_t tcalls[6] = {};
+  std::string err;
+
+  int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    err = buf;
+    return code;
+  }
+  hipEvent_t ev_get() {
+    if (ev_pool.empty()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      return e;
+    }
+    hipEvent_t e = ev_pool.back();
+    ev_pool.pop_back();
+    return e;
+  }
+  // brackets a launch group on stream s when timing is on
+  struct Range {
+    massive_ctx* c;
+    hipStream_t s;
+    int group;
+    hipEvent_t a = nullptr;
+    Range(massive_ctx* c_, hipStream_t s_, int g) : c(c_), s(s_), group(g) {
+      if (c->timing && (a = c->ev_get())) (void)hipEventRecord(a, s);
+    }
+    ~Range() {
+      if (!a) return;
+      hipEvent_t b = c->ev_get();
+      if (!b) return;
+      (void)hipEventRecord(b, s);
+      c->pending.push_back({a, b, group});
+    }
+  };
+  void resolve_timing() {
+    for (auto& r : pending) {
+      float ms = 0.f;
+      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+        tms[r.group] += ms;
+        tcalls[r.group] += 1;
+      }
+      ev_pool.push_back(r.a);
+      ev_pool.push_back(r.b);
+    }
+    pending.clear();
+  }
+};
+
+#define CK(call)                                                                          \
+  do {                                                                                    \
+    hipError_t e_ = (call);                                                               \
+    if (e_ != hipSuccess) return c->fail(MASSIVE_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+#define CKA(ptr, bytes)                                                                   \
+  do {                                                                                    \
+    size_t b_ = (size_t)(bytes);                                                          \
+    if (hipMalloc((void**)&(ptr), b_ ? b_ : 16) != hipSuccess)                            \
+      return c->fail(MASSIVE_ENOMEM, "hipMalloc of %zu bytes for %s failed", b_, #ptr);   \
+  } while (0)
+
+namespace {
+
+// one stable LSD pass: (kin, vin) -> (kout, vout) by 8-bit digit at `shift`
+int sort_pass(massive_ctx* c, hipStream_t s, const uint32_t* kin, const int32_t* vin, const int64_t* n_ptr,
+              int64_t n_const, int64_t bound, int shift, uint32_t* kout, int32_t* vout) {
+  const int64_t nb = std::max<int64_t>(1, cdiv(bound, ms::kSortTile));
+  ms::k_sort_hist<<<(unsigned)nb, ms::kSortNT, 0, s>>>(kin, n_ptr, n_const, bound, shift, nb, c->d_hist);
+  const int64_t len = 256 * nb, nb2 = std::max<int64_t>(1, cdiv(len, ms::kScanTile));
+  ms::k_tile_reduce<<<(unsigned)nb2, ms::kScanNT, 0, s>>>(c->d_hist, len, c->d_part);
+  ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nb2, nullptr, nullptr);
+  ms::k_tile_scan<<<(unsigned)nb2, ms::kScanNT, 0, s>>>(c->d_hist, len, c->d_part);
+  ms::k_sort_scatter<<<(unsigned)nb, ms::kSortNT, 0, s>>>(kin, vin, n_ptr, n_const, bound, shift, nb, c->d_hist, kout,
+                                                          vout);
+  return MASSIVE_OK;
+}
+
+// four passes of 8 bits; the result lands in (k0, v0), or its values in
+// `vals_final` if given.
+int sort_u32(massive_ctx* c, hipStream_t s, const int64_t* n_ptr, int64_t n_const, int64_t bound,
+             int32_t* vals_final) {
+  sort_pass(c, s, c->d_k0, c->d_v0, n_ptr, n_const, bound, 0, c->d_k1, c->d_v1);
+  sort_pass(c, s, c->d_k1, c->d_v1, n_ptr, n_const, bound, 8, c->d_k0, c->d_v0);
+  sort_pass(c, s, c->d_k0, c->d_v0, n_ptr, n_const, bound, 16, c->d_k1, c->d_v1);
+  sort_pass(c, s, c->d_k1, c->d_v1, n_ptr, n_const, bound, 24, c->d_k0, vals_final ? vals_final : c->d_v0);
+  return MASSIVE_OK;
+}
+
+bool device_visible(const void* p) {
+  hipPointerAttribute_t at;
+  if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return at.type == hipMemoryTypeDevice || at.type == hipMemoryTypeManaged || at.type == hipMemoryTypeHost ||
+         at.devicePointer != nullptr;
+}
+
+// the flattened gather, specialised on the widest vector the row allows
+enum GatherKind { kHbm, kMiss, kRefill };
+
+// The flattened row gather, specialised on the widest vector the row and
+// both base pointers allow. max_blocks bounds the grid: host-link gathers
+// use a few CUs (16 blocks reach the link's rate; more only congest the
+// fabric that HBM traffic also needs).
+void launch_gather(GatherKind kind, hipStream_t s, const int2* list, const int64_t* count, const uint8_t* src,
+                   uint8_t* dst, int64_t rb, int64_t max_rows, int64_t max_blocks) {
+  int vec = 4;
+  if (rb % 16 == 0 && ((uintptr_t)src % 16) == 0 && ((uintptr_t)dst % 16) == 0)
+    vec = 16;
+  else if (rb % 8 == 0 && ((uintptr_t)src % 8) == 0 && ((uintptr_t)dst % 8) == 0)
+    vec = 8;
+  const uint32_t cpr = (uint32_t)(rb / vec);
+  const uint64_t magic = cpr > 1 ? (~0ull) / cpr + 1 : 0;
+  const int64_t chunks = std::max<int64_t>(max_rows, 1) * cpr;
+  const unsigned grid = grid_for(chunks / 4, 256, max_blocks);
+#define MS_LAUNCH(K, V) ms::K<V><<<grid, 256, 0, s>>>(list, count, src, dst, rb, cpr, magic)
+#define MS_KIND(V)                         \
+  do {                                     \
+    if (kind == kHbm)                      \
+      MS_LAUNCH(k_gather_hbm, V);          \
+    else if (kind == kMiss)                \
+      MS_LAUNCH(k_gather_miss, V);         \
+    else                                   \
+      MS_LAUNCH(k_refill, V);              \
+  } while (0)
+  if (vec == 16)
+    MS_KIND(ms::v4u);
+  else if (vec == 8)
+    MS_KIND(ms::v2u);
+  else
+    MS_KIND(unsigned int);
+#undef MS_KIND
+#undef MS_LAUNCH
+}
+
+void free_ctx(massive_ctx* c) {
+  if (!c) return;
+  (void)hipDeviceSynchronize();
+  void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
+                 c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
+                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list, c->d_E, c->d_R, c->d_fill,
+                 c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist};
+  for (void* p : dev)
+    if (p) (void)hipFree(p);
+  if (c->h_sz) (void)hipHostFree(c->h_sz);
+  if (c->h_rs) (void)hipHostFree(c->h_rs);
+  for (hipEvent_t e : {c->ev_classified, c->ev_miss_done, c->ev_swap_done, c->ev_refill_done})
+    if (e) (void)hipEventDestroy(e);
+  for (auto& r : c->pending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->s_miss) (void)hipStreamDestroy(c->s_miss);
+  if (c->s_copy) (void)hipStreamDestroy(c->s_copy);
+  delete c;
+}
+
+int init_impl(massive_ctx* c, const massive_init_args* a) {
+  c->L = a->L;
+  c->H = a->H;
+  c->R = (int64_t)a->L + a->H;
+  c->rb = a->row_bytes;
+  c->K = a->K;
+  for (int k = 0; k < a->K; ++k) c->fo[k] = a->fanout[k];
+  c->pct = a->buffer_pct;
+  c->gamma = a->gamma;
+  c->delta = a->delta;
+  c->seed = a->seed;
+  c->nnz = a->indptr[c->R];
+  c->cap = (int64_t)a->H * a->buffer_pct / 100;
+  c->hcap = 64;
+  while (c->hcap < 2 * c->cap) c->hcap <<= 1;
+  c->hmask = (uint32_t)(c->hcap - 1);
+  c->W = cdiv(c->R, 32);
+  c->sort_cap = std::max<int64_t>(std::max<int64_t>(c->H, c->cap), 1);
+  c->pmax = std::max(cdiv(c->R, ms::kScanTile), cdiv(256 * cdiv(c->sort_cap, ms::kSortTile), ms::kScanTile));
+  c->pmax = std::max<int64_t>(c->pmax, cdiv(c->W, ms::kScanTile)) + 8;
+  // Eq. 1 with S_E at its initial value 1: alpha = gamma^delta in fp32 products
+  float al = 1.0f;
+  for (int32_t i = 0; i < a->delta; ++i) al = al * a->gamma;
+  c->alpha = al;
+
+  if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
+  c->s_main = (hipStream_t)a->stream;
+  CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
+  CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
+  for (hipEvent_t* e : {&c->ev_classified, &c->ev_miss_done, &c->ev_swap_done, &c->ev_refill_done})
+    CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+
+  // the pinned store must be mapped into the device address space
+  {
+    void* dp = nullptr;
+    if (c->H > 0) {
+      if (hipHostGetDevicePointer(&dp, const_cast<void*>(a->halo_store), 0) != hipSuccess || !dp)
+        return c->fail(MASSIVE_EINVAL, "halo_store is not pinned host memory (allocate it with hipHostMalloc / "
+                                       "torch pin_memory=True)");
+    }
+    c->d_store = (const uint8_t*)dp;
+  }
+
+  const int64_t R = c->R, H = c->H, cap = c->cap, rb = c->rb;
+  CKA(c->d_indptr, (R + 1) * 8);
+  CKA(c->d_indices, c->nnz * 4);
+  CKA(c->d_slab, (c->L + cap) * rb);
+  CKA(c->d_slot_id, cap * 4);
+  CKA(c->d_S_E, cap * 4);
+  CKA(c->d_hitcnt, cap * 4);
+  CKA(c->d_S_A, H * 4);
+  CKA(c->d_rank_of, H * 4);
+  CKA(c->d_h_of_rank, H * 4);
+  CKA(c->d_tab, c->hcap * 8);
+  CKA(c->d_pos_of, R * 4);
+  CKA(c->d_bits, (c->W + 4) * 4);
+  CKA(c->d_sz, sizeof(ms::StepSizes));
+  CKA(c->d_rs, sizeof(ms::RoundState));
+  CKA(c->d_part, c->pmax * 4);
+  CKA(c->d_part2, c->pmax * 4);
+  CKA(c->d_hbm_list, R * 8);
+  CKA(c->d_miss_list, R * 8);
+  CKA(c->d_E, cap * 4);
+  CKA(c->d_R, cap * 4);
+  CKA(c->d_fill, cap * 8);
+  CKA(c->d_k0, c->sort_cap * 4);
+  CKA(c->d_k1, c->sort_cap * 4);
+  CKA(c->d_v0, c->sort_cap * 4);
+  CKA(c->d_v1, c->sort_cap * 4);
+  CKA(c->d_hist, 256 * cdiv(c->sort_cap, ms::kSortTile) * 4);
+  CKA(c->d_ghist, 256 * 4);
+  if (hipHostMalloc((void**)&c->h_sz, sizeof(ms::StepSizes), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_rs, sizeof(ms::RoundState), hipHostMallocDefault) != hipSuccess)
+    return c->fail(MASSIVE_ENOMEM, "hipHostMalloc of the size mailboxes failed");
+
+  hipStream_t s = c->s_main;
+  CK(hipMemcpyAsync(c->d_indptr, a->indptr, (R + 1) * 8, hipMemcpyHostToDevice, s));
+  if (c->nnz) CK(hipMemcpyAsync(c->d_indices, a->indices, c->nnz * 4, hipMemcpyHostToDevice, s));
+  if (c->L) CK(hipMemcpyAsync(c->d_slab, a->local_feat, (int64_t)c->L * rb, hipMemcpyHostToDevice, s));
+  {
+    CK(hipMemsetAsync(&c->d_rs->bad, 0, 4, s));
+    ms::k_validate_csr<<<grid_for(std::max(R, c->nnz), 256, 8192), 256, 0, s>>>(c->d_indptr, R, c->d_indices, c->nnz,
+                                                                                &c->d_rs->bad);
+    CK(hipMemcpyAsync(&c->h_rs->bad, &c->d_rs->bad, 4, hipMemcpyDeviceToHost, s));
+    CK(hipStreamSynchronize(s));
+    if (c->h_rs->bad)
+      return c->fail(MASSIVE_EINVAL, (c->h_rs->bad & 2) ? "indices has ids outside [0, L+H)"
+                                                         : "indptr is not non-decreasing");
+  }
+  CK(hipMemsetAsync(c->d_pos_of, 0xFF, R * 4, s));
+  CK(hipMemsetAsync(c->d_bits, 0, (c->W + 4) * 4, s));
+  CK(hipMemsetAsync(c->d_ghist, 0, 256 * 4, s));
+
+  if (H > 0) {
+    // halo rank: (degree desc, global id asc) by two stable radix sorts
+    int32_t* d_gid = nullptr;
+    int64_t* d_deg = nullptr;
+    CKA(d_gid, H * 4);
+    CKA(d_deg, H * 8);
+    CK(hipMemcpyAsync(d_gid, a->halo_gid, H * 4, hipMemcpyHostToDevice, s));
+    CK(hipMemcpyAsync(d_deg, a->halo_degree, H * 8, hipMemcpyHostToDevice, s));
+    ms::k_rank_keys_lo<<<grid_for(H, 256), 256, 0, s>>>(d_gid, H, c->d_k0, c->d_v0);
+    sort_u32(c, s, nullptr, H, H, nullptr);
+    ms::k_rank_keys_hi<<<grid_for(H, 256), 256, 0, s>>>(d_deg, c->d_v0, H, c->d_k0);
+    sort_u32(c, s, nullptr, H, H, c->d_h_of_rank);
+    ms::k_rank_finish<<<grid_for(H, 256), 256, 0, s>>>(c->d_h_of_rank, H, c->d_rank_of);
+    ms::k_fill<float><<<grid_for(H, 256), 256, 0, s>>>(c->d_S_A, H, 0.0f);
+    CK(hipStreamSynchronize(s));
+    (void)hipFree(d_gid);
+    (void)hipFree(d_deg);
+  }
+  ms::k_fill<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty);
+  if (cap > 0) {
+    ms::k_init_buffer<<<grid_for(cap, 256), 256, 0, s>>>(c->d_h_of_rank, cap, c->L, c->d_slot_id, c->d_S_E,
+                                                         c->d_hitcnt, c->d_S_A, c->d_fill);
+    ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap);
+    // the cap best-ranked rows arrive over the host link
+    c->h_rs->k = cap;
+    CK(hipMemcpyAsync(&c->d_rs->k, &c->h_rs->k, 8, hipMemcpyHostToDevice, s));
+    launch_gather(kRefill, s, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, rb, cap, c->host_blocks);
+  }
+  CK(hipGetLastError());
+  CK(hipStreamSynchronize(s));
+  return MASSIVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int massive_init(const massive_init_args* a, massive_ctx** out) {
+  g_init_error.clear();
+  if (!out) {
+    g_init_error = "out is NULL";
+    return MASSIVE_EINVAL;
+  }
+  *out = nullptr;
+  auto bad = [](const char* m) {
+    g_init_error = m;
+    return MASSIVE_EINVAL;
+  };
+  if (!a) return bad("args is NULL");
+  if (a->L < 0 || a->H < 0 || (int64_t)a->L + a->H <= 0) return bad("need L >= 0, H >= 0, L + H > 0");
+  if (!a->indptr || !a->indices) return bad("indptr / indices are NULL");
+  if (a->L > 0 && !a->local_feat) return bad("local_feat is NULL");
+  if (a->H > 0 && (!a->halo_store || !a->halo_gid || !a->halo_degree)) return bad("halo arrays are NULL");
+  if (a->row_bytes <= 0 || a->row_bytes % 4) return bad("row_bytes must be a positive multiple of 4");
+  if (a->K < 1 || a->K > MASSIVE_MAX_HOPS) return bad("K must be in 1..8");
+  for (int k = 0; k < a->K; ++k)
+    if (a->fanout[k] < 1) return bad("every fanout must be >= 1");
+  if (a->buffer_pct < 0 || a->buffer_pct > 100) return bad("buffer_pct must be in 0..100");
+  if (!(a->gamma > 0.0f && a->gamma <= 1.0f)) return bad("gamma must be in (0, 1]");
+  if (a->delta < 1) return bad("delta must be >= 1");
+  const int64_t R = (int64_t)a->L + a->H;
+  if (a->indptr[0] != 0 || a->indptr[R] < 0) return bad("indptr must start at 0");
+  massive_ctx* c = new (std::nothrow) massive_ctx();
+  if (!c) return bad("out of host memory");
+  int rc = init_impl(c, a);
+  if (rc != MASSIVE_OK) {
+    g_init_error = c->err;
+    free_ctx(c);
+    return rc;
+  }
+  *out = c;
+  return MASSIVE_OK;
+}
+
+int massive_output_bounds(const massive_ctx* c, int32_t n_seeds, int64_t* n_bound, int64_t* e_bound) {
+  if (!c || !n_bound || !e_bound || n_seeds < 0) return MASSIVE_EINVAL;
+  n_bound[0] = std::min<int64_t>(n_seeds, c->L);
+  for (int k = 0; k < c->K; ++k) {
+    e_bound[k] = n_bound[k] * c->fo[k];
+    n_bound[k + 1] = std::min<int64_t>(c->R, n_bound[k] + e_bound[k]);
+  }
+  return MASSIVE_OK;
+}
+
+int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
+  if (!c) return MASSIVE_EINVAL;
+  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier device failure");
+  if (!io || n0 < 0 || (n0 > 0 && !seeds)) return c->fail(MASSIVE_EINVAL, "bad seeds / batch arguments");
+  if (c->pending_round) return c->fail(MASSIVE_ESTATE, "massive_evict_step was not called after the last step");
+  if (n0 > c->L) return c->fail(MASSIVE_EINVAL, "more seeds than local nodes");
+  int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
+  massive_output_bounds(c, n0, nb, eb);
+  if (!io->nodes || !io->mask || !io->feat) return c->fail(MASSIVE_EINVAL, "nodes / mask / feat are NULL");
+  if (io->nodes_cap < nb[c->K]) return c->fail(MASSIVE_ECAPACITY, "nodes_cap %lld < bound %lld",
+                                               (long long)io->nodes_cap, (long long)nb[c->K]);
+  for (int k = 0; k < c->K; ++k) {
+    if (!io->indptr[k] || !io->indices[k]) return c->fail(MASSIVE_EINVAL, "hop %d buffers are NULL", k + 1);
+    if (io->indptr_cap[k] < nb[k] + 1 || io->indices_cap[k] < eb[k])
+      return c->fail(MASSIVE_ECAPACITY, "hop %d buffers below the bound (%lld, %lld)", k + 1, (long long)(nb[k] + 1),
+                     (long long)eb[k]);
+    if (eb[k] >= (1ll << 31)) return c->fail(MASSIVE_EINVAL, "hop %d may emit 2^31 edges or more", k + 1);
+  }
+  if (c->t >= 0xFFFFFFFFll) return c->fail(MASSIVE_ESTATE, "step counter exhausted");
+  {
+    // every pointer the kernels dereference must be visible to the device
+    const void* ptrs[3 + 2 * MASSIVE_MAX_HOPS] = {io->nodes, io->mask, io->feat};
+    int np = 3;
+    if (n0 > 0) ptrs[np++] = seeds;
+    for (int k = 0; k < c->K; ++k) {
+      ptrs[np++] = io->indptr[k];
+      ptrs[np++] = io->indices[k];
+    }
+    for (int i = 0; i < np; ++i)
+      if (!device_visible(ptrs[i])) return c->fail(MASSIVE_EINVAL, "argument %d is not HIP-visible memory", i);
+  }
+
+  hipStream_t s = c->s_main;
+  const uint32_t key0 = (uint32_t)c->seed, key1 = (uint32_t)(c->seed >> 32);
+  CK(hipMemsetAsync(c->d_sz, 0, sizeof(ms::StepSizes), s));
+  {
+    massive_ctx::Range tr(c, s, 0);
+    if (n0 > 0)
+      ms::k_seed_init<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, io->nodes, c->d_pos_of, c->d_sz);
+    for (int k = 1; k <= c->K; ++k) {
+      const int64_t nprev = nb[k - 1];
+      const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
+      ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, c->d_sz, k, c->fo[k - 1],
+                                                              io->indptr[k - 1], c->d_part);
+      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbk, &c->d_sz->e[k - 1], nullptr);
+      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_sz, k, io->indptr[k - 1], c->d_part);
+      ms::SampleArgs sa;
+      sa.csr_indptr = c->d_indptr;
+      sa.csr_indices = c->d_indices;
+      sa.nodes = io->nodes;
+      sa.sz = c->d_sz;
+      sa.bptr = io->indptr[k - 1];
+      sa.out = io->indices[k - 1];
+      sa.hop = k;
+      sa.fo = c->fo[k - 1];
+      sa.t = (uint32_t)c->t;
+      sa.key0 = key0;
+      sa.key1 = key1;
+      sa.err = &c->d_sz->status;
+      ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
+                     s>>>(sa);
+      ms::k_mark_new<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], c->d_sz, k, c->d_pos_of,
+                                                               c->d_bits);
+      const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
+      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, c->d_part);
+      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbw, &c->d_sz->n[k], &c->d_sz->n[k - 1]);
+      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, k, c->d_part, io->nodes,
+                                                             c->d_pos_of);
+      ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], c->d_sz, k, c->d_pos_of);
+    }
+  }
+  {
+    massive_ctx::Range tr(c, s, 1);
+    ms::ClassifyArgs ca;
+    ca.nodes = io->nodes;
+    ca.sz = c->d_sz;
+    ca.K = c->K;
+    ca.L = c->L;
+    ca.tab = c->d_tab;
+    ca.tmask = c->hmask;
+    ca.hitcnt = c->d_hitcnt;
+    ca.S_A = c->d_S_A;
+    ca.pos_of = c->d_pos_of;
+    ca.mask = io->mask;
+    ca.hbm_list = c->d_hbm_list;
+    ca.miss_list = c->d_miss_list;
+    ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, 4096), ms::kClsNT, 0, s>>>(ca);
+  }
+  // HBM rows first, at full bandwidth; the host-link rows follow on the side
+  // stream (concurrent host reads would throttle the HBM gather).
+  if (c->refill_pending) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
+  {
+    massive_ctx::Range tr(c, s, 2);
+    launch_gather(kHbm, s, c->d_hbm_list, &c->d_sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
+  }
+  CK(hipEventRecord(c->ev_classified, s));
+  CK(hipStreamWaitEvent(c->s_miss, c->ev_classified, 0));
+  {
+    massive_ctx::Range tr(c, c->s_miss, 3);
+    if (c->H > 0)
+      launch_gather(kMiss, c->s_miss, c->d_miss_list, &c->d_sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb,
+                    nb[c->K], c->host_blocks);
+  }
+  CK(hipEventRecord(c->ev_miss_done, c->s_miss));
+  CK(hipStreamWaitEvent(s, c->ev_miss_done, 0));
+  CK(hipMemcpyAsync(c->h_sz, c->d_sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, s));
+  CK(hipGetLastError());
+  CK(hipStreamSynchronize(s));
+  c->refill_pending = false;
+  const ms::StepSizes& z = *c->h_sz;
+  if (z.status & 3) {
+    if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of);
+    CK(hipStreamSynchronize(s));
+    return c->fail(MASSIVE_EINVAL, (z.status & 1) ? "a seed is not a local node id" : "a seed is repeated");
+  }
+  if (z.status) {
+    c->broken = true;
+    return c->fail(MASSIVE_EHIP, "sampler could not isolate a candidate set (status %d)", z.status);
+  }
+  for (int k = 0; k <= c->K; ++k) io->n[k] = z.n[k];
+  for (int k = 0; k < c->K; ++k) io->e[k] = z.e[k];
+  io->local = z.local;
+  io->hits = z.hits;
+  io->misses = z.misses;
+  c->t += 1;
+  c->pending_round = true;
+  if (c->timing) c->resolve_timing();
+  return MASSIVE_OK;
+}
+
+int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t* replaced, int64_t* k_out) {
+  if (!c || !k_out) return MASSIVE_EINVAL;
+  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier device failure");
+  if (!c->pending_round) return c->fail(MASSIVE_ESTATE, "no sampled step owes an eviction round");
+  c->pending_round = false;
+  *k_out = 0;
+  const int64_t tl = c->t - 1;
+  if (!(tl > 0 && tl % c->delta == 0)) return MASSIVE_OK;
+  if (c->cap == 0) return MASSIVE_OK;
+  for (const void* p : {(const void*)evicted, (const void*)slots, (const void*)replaced})
+    if (p && !device_visible(p)) return c->fail(MASSIVE_EINVAL, "an eviction output is not HIP-visible memory");
+  hipStream_t s = c->s_main;
+  const int64_t cap = c->cap, H = c->H;
+  int64_t kk = 0;
+  {
+    massive_ctx::Range tr(c, s, 4);
+    ms::k_materialize<<<grid_for(cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, cap, (int32_t)(c->t - c->mat_t),
+                                                          c->gamma);
+    c->mat_t = c->t;
+    CK(hipMemsetAsync(c->d_rs, 0, sizeof(ms::RoundState), s));
+    const int64_t nbe = std::max<int64_t>(1, cdiv(cap, ms::kScanTile));
+    ms::k_evict_count<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part);
+    ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbe, &c->d_rs->nE, nullptr);
+    ms::k_evict_emit<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part, c->d_E);
+    ms::k_count_candidates<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, &c->d_rs->nC);
+    CK(hipMemcpyAsync(c->h_rs, c->d_rs, sizeof(ms::RoundState), hipMemcpyDeviceToHost, s));
+    CK(hipStreamSynchronize(s));
+    const int64_t nE = c->h_rs->nE, nC = c->h_rs->nC;
+    kk = std::min(nE, nC);
+    if (kk > 0) {
+      c->h_rs->k = kk;
+      c->h_rs->need = kk;
+      c->h_rs->prefix = 0;
+      c->h_rs->pmask = 0;
+      CK(hipMemcpyAsync(c->d_rs, c->h_rs, sizeof(ms::RoundState), hipMemcpyHostToDevice, s));
+      if (kk < nE) {
+        // fewer candidates than evictions: keep the kk slots of smallest (S_E, rank)
+        const int64_t* nEp = &c->d_rs->nE;
+        ms::k_esel_keys_lo<<<grid_for(nE, 256), 256, 0, s>>>(c->d_E, nEp, c->d_slot_id, c->d_rank_of, c->d_k0, c->d_v0);
+        sort_u32(c, s, nEp, 0, cap, nullptr);
+        ms::k_esel_keys_hi<<<grid_for(nE, 256), 256, 0, s>>>(c->d_v0, nEp, c->d_S_E, c->d_k0);
+        sort_u32(c, s, nEp, 0, cap, nullptr);
+        ms::k_esel_keys_slot<<<grid_for(kk, 256), 256, 0, s>>>(c->d_v0, &c->d_rs->k, c->d_k0);
+        sort_u32(c, s, &c->d_rs->k, 0, cap, c->d_E);
+      }
+      ms::k_fill<int32_t><<<grid_for(kk, 256), 256, 0, s>>>(c->d_R, kk, -1);
+      // radix select of the kk-th candidate key, 8 bits per pass
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        ms::k_select_hist<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, c->d_rs, shift, c->d_ghist);
+        ms::k_select_pick<<<1, 256, 0, s>>>(c->d_rs, c->d_ghist, shift);
+      }
+      const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
+      ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, c->d_rs, c->d_part,
+                                                             c->d_part2);
+      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbh, &c->d_rs->n_lt, nullptr);
+      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part2, nbh, &c->d_rs->n_eq, nullptr);
+      ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, c->d_rs, c->d_part,
+                                                            c->d_part2, c->d_k0, c->d_v0, c->d_R);
+      // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
+      sort_u32(c, s, &c->d_rs->n_lt, 0, cap, c->d_R);
+      ms::k_swap<<<grid_for(kk, 256), 256, 0, s>>>(c->d_E, c->d_R, &c->d_rs->k, c->L, cap, c->H, c->d_slot_id,
+                                                   c->d_S_E, c->d_S_A, evicted, slots, replaced, c->d_fill,
+                                                   &c->d_rs->bad);
+      ms::k_fill<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty);
+      ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap);
+    }
+  }
+  if (kk > 0) {
+    CK(hipMemcpyAsync(&c->h_rs->bad, &c->d_rs->bad, 4, hipMemcpyDeviceToHost, s));
+    CK(hipStreamSynchronize(s));
+    if (c->h_rs->bad) {
+      c->broken = true;
+      return c->fail(MASSIVE_EHIP, "eviction round produced inconsistent indices");
+    }
+    CK(hipEventRecord(c->ev_swap_done, s));
+    CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
+    {
+      massive_ctx::Range tr(c, c->s_copy, 5);
+      launch_gather(kRefill, c->s_copy, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, c->rb, kk, c->host_blocks);
+    }
+    CK(hipEventRecord(c->ev_refill_done, c->s_copy));
+    c->refill_pending = true;
+  }
+  CK(hipGetLastError());
+  *k_out = kk;
+  return MASSIVE_OK;
+}
+
+int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, int64_t* t) {
+  if (!c) return MASSIVE_EINVAL;
+  hipStream_t s = c->s_main;
+  if (c->cap > 0 && c->t > c->mat_t) {
+    ms::k_materialize<<<grid_for(c->cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, c->cap,
+                                                             (int32_t)(c->t - c->mat_t), c->gamma);
+    c->mat_t = c->t;
+  }
+  if (slot_id && c->cap) CK(hipMemcpyAsync(slot_id, c->d_slot_id, c->cap * 4, hipMemcpyDeviceToHost, s));
+  if (S_E && c->cap) CK(hipMemcpyAsync(S_E, c->d_S_E, c->cap * 4, hipMemcpyDeviceToHost, s));
+  if (S_A && c->H) CK(hipMemcpyAsync(S_A, c->d_S_A, (int64_t)c->H * 4, hipMemcpyDeviceToHost, s));
+  CK(hipStreamSynchronize(s));
+  if (t) *t = c->t;
+  return MASSIVE_OK;
+}
+
+int massive_get_buffer_rows(massive_ctx* c, void* out) {
+  if (!c || (!out && c->cap)) return MASSIVE_EINVAL;
+  if (c->refill_pending) CK(hipStreamWaitEvent(c->s_main, c->ev_refill_done, 0));
+  if (c->cap)
+    CK(hipMemcpyAsync(out, c->d_slab + (int64_t)c->L * c->rb, c->cap * c->rb, hipMemcpyDeviceToHost, c->s_main));
+  CK(hipStreamSynchronize(c->s_main));
+  return MASSIVE_OK;
+}
+
+int massive_info(const massive_ctx* c, int64_t* cap, float* alpha) {
+  if (!c) return MASSIVE_EINVAL;
+  if (cap) *cap = c->cap;
+  if (alpha) *alpha = c->alpha;
+  return MASSIVE_OK;
+}
+
+int massive_set_timing(massive_ctx* c, int enable) {
+  if (!c) return MASSIVE_EINVAL;
+  CK(hipDeviceSynchronize());
+  c->resolve_timing();
+  c->timing = enable != 0;
+  for (int i = 0; i < 6; ++i) {
+    c->tms[i] = 0.0;
+    c->tcalls[i] = 0;
+  }
+  return MASSIVE_OK;
+}
+
+int massive_get_timing(massive_ctx* c, double* out_ms, int64_t* out_calls) {
+  if (!c) return MASSIVE_EINVAL;
+  CK(hipStreamSynchronize(c->s_main));
+  CK(hipStreamSynchronize(c->s_miss));
+  CK(hipStreamSynchronize(c->s_copy));
+  c->resolve_timing();
+  for (int i = 0; i < 6; ++i) {
+    if (out_ms) out_ms[i] = c->tms[i];
+    if (out_calls) out_calls[i] = c->tcalls[i];
+  }
+  return MASSIVE_OK;
+}
+
+int massive_destroy(massive_ctx* c) {
+  free_ctx(c);
+  return MASSIVE_OK;
+}
+
+const char* massive_last_error(const massive_ctx* c) {
+  if (!c) return g_init_error.c_str();
+  return c->err.c_str();
+}
+
+}  // extern "C"

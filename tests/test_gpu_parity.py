@@ -1,0 +1,130 @@
+"""GPU parity: libmassive (through the C ABI) against the oracle, element by
+element: sampled blocks, frontier, masks, gathered rows, eviction sets and
+scores. Sizes span several tiles and ragged tails; the oracle finishes each in
+seconds."""
+import numpy as np
+import pytest
+
+from gpu_util import log, make_gpu, pinned_store, require_gpu, run_parity, to_dev
+from helpers import tiny_problem, workload_problem
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def test_tiny_graphs():
+    total = 0
+    for seed in (1, 2, 3):
+        prob = tiny_problem(n_local=6, n_halo=9, p=0.4, seed=seed, fanout=(2, 1), buffer_pct=34, delta=2, gamma=0.5)
+        rng = np.random.default_rng(seed)
+        seeds = [rng.permutation(prob.L)[:1].astype(np.int32) for _ in range(16)]
+        rounds, _, _ = run_parity("tiny%d" % seed, prob, lambda t: seeds[t], 16)
+        total += rounds
+    assert total >= 3
+
+
+def test_cl10k_full_run():
+    prob, sched, w = workload_problem("cl10k")
+    rounds, _, _ = run_parity("cl10k", prob, sched.seeds, w.steps, buffer_rows_every=5)
+    assert rounds >= 5
+
+
+@pytest.mark.parametrize("over", [dict(gamma=0.8, delta=3, buffer_pct=50),
+                                  dict(gamma=0.7, delta=2, buffer_pct=80),    # fewer candidates than evictions
+                                  dict(buffer_pct=100, delta=2),                # no candidates at all
+                                  dict(buffer_pct=0, delta=2),                  # empty buffer
+                                  dict(gamma=1.0, delta=2),                     # nothing ever decays below alpha
+                                  dict(fanout=(40, 30, 2), delta=5)])           # rows up to 320 long, long-row path
+def test_cl10k_variants(over):
+    prob, sched, w = workload_problem("cl10k", **over)
+    run_parity("cl10k%s" % sorted(over.items()), prob, sched.seeds, 20, buffer_rows_every=4)
+
+
+def test_cl170k():
+    prob, sched, w = workload_problem("cl170k")
+    rounds, _, _ = run_parity("cl170k", prob, sched.seeds, 34, state_every=4)
+    assert rounds == 1  # t = 16 finds no slot below alpha; t = 32 evicts
+
+
+def test_cl2m45_short_interval():
+    # products-sized graph, 3 hops, hub rows of ~11K neighbours; delta lowered
+    # so that two rounds fit in a short run.
+    prob, sched, w = workload_problem("cl2m45", delta=2)
+    rounds, _, _ = run_parity("cl2m45", prob, sched.seeds, 5, state_every=2)
+    assert rounds == 2
+
+
+def test_cl2m45_bf16_rows():
+    # 200-byte bf16 rows (8-byte vectors), fanout (20,15,10), f = 50%, gamma 0.8;
+    # batch lowered to keep the oracle within seconds.
+    prob, sched, w = workload_problem("cl2m45_bf16", batch=512)
+    from synth import Schedule
+    sch = Schedule(prob.L, w.train_pct, 512, w.seed)
+    rounds, _, _ = run_parity("cl2m45_bf16", prob, sch.seeds, 5, state_every=2)
+    assert rounds == 1
+
+
+def test_empty_and_ragged_batches():
+    prob, sched, w = workload_problem("cl10k", delta=2)
+    sizes = [0, 1, 63, 64, 65, 250, 0, 7, 129, 1]
+    rng = np.random.default_rng(5)
+    seeds = [rng.permutation(prob.L)[:n].astype(np.int32) for n in sizes]
+    run_parity("cl10k ragged", prob, lambda t: seeds[t], len(sizes), batch_max=250)
+
+
+def test_invalid_seeds_leave_state_unchanged():
+    from paper_2410_22697_amd import MassiveError
+    prob, sched, w = workload_problem("cl10k")
+    gm = make_gpu(prob)
+    orc = prob.oracle()
+    bb = gm.alloc_batch(256)
+    for bad in ([prob.L], [-1], [3, 3]):
+        log("invalid seeds %s" % bad)
+        with pytest.raises(MassiveError) as ei:
+            gm.sample(to_dev(np.array(bad, np.int32)), bb)
+        assert ei.value.code == -1
+    log("valid step after the rejections")
+    from gpu_util import compare_step
+    st = orc.sample(sched.seeds(0))
+    res = gm.sample(to_dev(sched.seeds(0)), bb)
+    compare_step("after invalid", st, res, bb, len(prob.fanout))
+    with pytest.raises(MassiveError) as ei:
+        gm.sample(to_dev(sched.seeds(1)), bb)         # evict call is owed first
+    assert ei.value.code == -5
+
+
+def test_output_capacity_is_checked():
+    from paper_2410_22697_amd import MassiveError
+    prob, sched, w = workload_problem("cl10k")
+    gm = make_gpu(prob)
+    bb = gm.alloc_batch(100)
+    with pytest.raises(MassiveError) as ei:
+        gm.sample(to_dev(sched.seeds(0)), bb)         # 250 seeds > bound of 100
+    assert ei.value.code == -2
+
+
+def test_deterministic_bytes():
+    import torch
+    prob, sched, w = workload_problem("cl170k")
+    outs = []
+    store = pinned_store(prob)
+    for rep in range(2):
+        log("determinism run %d" % rep)
+        gm = make_gpu(prob, store=store)
+        bb = gm.alloc_batch(w.batch)
+        digest = []
+        for t in range(18):
+            r = gm.sample(to_dev(sched.seeds(t)), bb)
+            nK = r.n[-1]
+            digest.append((bb.nodes[:nK].cpu().numpy().tobytes(), bb.feat[:nK].cpu().numpy().tobytes(),
+                           bb.indices[2][:r.e[2]].cpu().numpy().tobytes(), bb.mask[:nK].cpu().numpy().tobytes()))
+            gm.evict_step()
+        sid, se, sa, _ = gm.state()
+        outs.append((digest, sid.tobytes(), se.tobytes(), sa.tobytes()))
+        gm.close()
+        torch.cuda.synchronize()
+    assert outs[0] == outs[1]
