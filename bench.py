@@ -57,6 +57,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--threads", type=int, default=None)
+    ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each partition's "
@@ -81,9 +84,20 @@ def main():
     seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
     torch.cuda.synchronize()
 
+    if args.copy_probe:
+        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy probe: 256 MiB device-to-device copy done")
+        del a, b
+
     first_steps = []  # digests of the first steps, checked against the oracle below
     for t in range(args.warmup):
         r = gm.sample(seeds_dev[t], bb)
+        if args.log_steps:
+            log("step %d local %d hits %d misses %d rows %d" % (t, r.local, r.hits, r.misses, r.n[-1]))
         if t < 2:
             nK = r.n[-1]
             first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
@@ -101,6 +115,8 @@ def main():
         r = gm.sample(seeds_dev[t], bb)
         k = gm.evict_step()
         stats.append((r.local, r.hits, r.misses, r.n[-1]))
+        if args.log_steps:
+            log("step %d local %d hits %d misses %d rows %d" % (t, r.local, r.hits, r.misses, r.n[-1]))
         rounds += k > 0
         evicted += k
     torch.cuda.synchronize()

@@ -94,6 +94,7 @@ struct StepSizes {
   int64_t e[8];      // sampled edges per hop
   int64_t local, hits, misses;
   int64_t n_hbm, n_miss;  // lengths of the two gather lists
+  int64_t n_big[8];       // rows longer than the big-row threshold, per hop
   int32_t status;    // != 0: invalid seeds; later kernels of the step skip
   int32_t pad;
 };

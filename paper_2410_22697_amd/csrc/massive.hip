@@ -6,12 +6,14 @@
 // overlaps the next step's sampling (the next HBM gather waits for it).
 // All device memory is allocated in massive_init; the per-step calls do not
 // allocate.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -55,6 +57,9 @@ struct massive_ctx {
   int64_t pmax = 0;     // partials capacity
   int64_t sort_cap = 0; // radix sort capacity
   int64_t host_blocks = 16;  // grid of the host-link gathers
+  double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
+  int32_t* d_big = nullptr;             // big-row list of the current hop
+  int64_t big_min = ms::kBigRow;        // rows longer than this use the 16-wave kernel
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
   hipEvent_t ev_classified = nullptr, ev_miss_done = nullptr, ev_swap_done = nullptr, ev_refill_done = nullptr;
@@ -139,6 +144,15 @@ struct massive_ctx {
       c->pending.push_back({a, b, group});
     }
   };
+  // a start/stop pair that hipExtLaunchKernelGGL stamps around one dispatch
+  bool kernel_pair(hipEvent_t* a, hipEvent_t* b) {
+    *a = *b = nullptr;
+    if (!timing) return false;
+    *a = ev_get();
+    *b = ev_get();
+    if (!*a || !*b) return false;
+    return true;
+  }
   void resolve_timing() {
     for (auto& r : pending) {
       float ms = 0.f;
@@ -210,8 +224,13 @@ enum GatherKind { kHbm, kMiss, kRefill };
 // both base pointers allow. max_blocks bounds the grid: host-link gathers
 // use a few CUs (16 blocks reach the link's rate; more only congest the
 // fabric that HBM traffic also needs).
-void launch_gather(GatherKind kind, hipStream_t s, const int2* list, const int64_t* count, const uint8_t* src,
-                   uint8_t* dst, int64_t rb, int64_t max_rows, int64_t max_blocks) {
+// With timing on, the dispatch itself is bracketed by hipExtLaunchKernelGGL's
+// start/stop events (no launch latency in the measured time).
+void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, const int2* list,
+                   const int64_t* count, const uint8_t* src, uint8_t* dst, int64_t rb, int64_t max_rows,
+                   int64_t max_blocks) {
+  hipEvent_t ea = nullptr, eb = nullptr;
+  const bool timed = c->kernel_pair(&ea, &eb);
   int vec = 4;
   if (rb % 16 == 0 && ((uintptr_t)src % 16) == 0 && ((uintptr_t)dst % 16) == 0)
     vec = 16;
@@ -221,7 +240,14 @@ void launch_gather(GatherKind kind, hipStream_t s, const int2* list, const int64
   const uint64_t magic = cpr > 1 ? (~0ull) / cpr + 1 : 0;
   const int64_t chunks = std::max<int64_t>(max_rows, 1) * cpr;
   const unsigned grid = grid_for(chunks / 4, 256, max_blocks);
-#define MS_LAUNCH(K, V) ms::K<V><<<grid, 256, 0, s>>>(list, count, src, dst, rb, cpr, magic)
+#define MS_LAUNCH(K, V)                                                                          \
+  do {                                                                                           \
+    if (timed)                                                                                   \
+      hipExtLaunchKernelGGL(ms::K<V>, dim3(grid), dim3(256), 0, s, ea, eb, 0, list, count, src, dst, rb, cpr, \
+                            magic);                                                              \
+    else                                                                                         \
+      ms::K<V><<<grid, 256, 0, s>>>(list, count, src, dst, rb, cpr, magic);                      \
+  } while (0)
 #define MS_KIND(V)                         \
   do {                                     \
     if (kind == kHbm)                      \
@@ -239,6 +265,7 @@ void launch_gather(GatherKind kind, hipStream_t s, const int2* list, const int64
     MS_KIND(unsigned int);
 #undef MS_KIND
 #undef MS_LAUNCH
+  if (timed) c->pending.push_back({ea, eb, group});
 }
 
 void free_ctx(massive_ctx* c) {
@@ -247,7 +274,7 @@ void free_ctx(massive_ctx* c) {
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
                  c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list, c->d_E, c->d_R, c->d_fill,
-                 c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist};
+                 c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   if (c->h_sz) (void)hipHostFree(c->h_sz);
@@ -288,8 +315,15 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   float al = 1.0f;
   for (int32_t i = 0; i < a->delta; ++i) al = al * a->gamma;
   c->alpha = al;
+  // sampler: about fo + 3 sqrt(fo) + 3 keys survive the first threshold
+  for (int k = 0; k < a->K; ++k) {
+    const double fo = a->fanout[k];
+    const double mu = std::min(fo + 3.0 * std::sqrt(fo) + 3.0, 0.5 * (fo + ms::kCandCap));
+    c->mu32[k] = mu * 4294967296.0;
+  }
 
   if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
+  if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
@@ -319,6 +353,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_h_of_rank, H * 4);
   CKA(c->d_tab, c->hcap * 8);
   CKA(c->d_pos_of, R * 4);
+  CKA(c->d_big, R * 4);
   CKA(c->d_bits, (c->W + 4) * 4);
   CKA(c->d_sz, sizeof(ms::StepSizes));
   CKA(c->d_rs, sizeof(ms::RoundState));
@@ -383,7 +418,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
     // the cap best-ranked rows arrive over the host link
     c->h_rs->k = cap;
     CK(hipMemcpyAsync(&c->d_rs->k, &c->h_rs->k, 8, hipMemcpyHostToDevice, s));
-    launch_gather(kRefill, s, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, rb, cap, c->host_blocks);
+    launch_gather(c, 5, kRefill, s, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, rb, cap, c->host_blocks);
   }
   CK(hipGetLastError());
   CK(hipStreamSynchronize(s));
@@ -413,7 +448,7 @@ int massive_init(const massive_init_args* a, massive_ctx** out) {
   if (a->row_bytes <= 0 || a->row_bytes % 4) return bad("row_bytes must be a positive multiple of 4");
   if (a->K < 1 || a->K > MASSIVE_MAX_HOPS) return bad("K must be in 1..8");
   for (int k = 0; k < a->K; ++k)
-    if (a->fanout[k] < 1) return bad("every fanout must be >= 1");
+    if (a->fanout[k] < 1 || a->fanout[k] > 256) return bad("every fanout must be in 1..256");
   if (a->buffer_pct < 0 || a->buffer_pct > 100) return bad("buffer_pct must be in 0..100");
   if (!(a->gamma > 0.0f && a->gamma <= 1.0f)) return bad("gamma must be in (0, 1]");
   if (a->delta < 1) return bad("delta must be >= 1");
@@ -484,8 +519,7 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
       const int64_t nprev = nb[k - 1];
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
       ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, c->d_sz, k, c->fo[k - 1],
-                                                              io->indptr[k - 1], c->d_part);
-      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbk, &c->d_sz->e[k - 1], nullptr);
+                                                              io->indptr[k - 1], c->d_part, c->d_big, c->big_min);
       ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_sz, k, io->indptr[k - 1], c->d_part);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
@@ -500,13 +534,16 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
       sa.key0 = key0;
       sa.key1 = key1;
       sa.err = &c->d_sz->status;
-      ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
+      sa.mu32 = c->mu32[k - 1];
+      sa.big_min = c->big_min;
+      sa.big_rows = c->d_big;
+      sa.row_waves = nprev;  // the big list never exceeds the frontier
+      sa.pos_of = c->d_pos_of;
+      sa.bits = c->d_bits;
+      ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
                      s>>>(sa);
-      ms::k_mark_new<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], c->d_sz, k, c->d_pos_of,
-                                                               c->d_bits);
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, c->d_part);
-      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbw, &c->d_sz->n[k], &c->d_sz->n[k - 1]);
+      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, k, c->d_part);
       ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, k, c->d_part, io->nodes,
                                                              c->d_pos_of);
       ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], c->d_sz, k, c->d_pos_of);
@@ -532,18 +569,12 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
   // HBM rows first, at full bandwidth; the host-link rows follow on the side
   // stream (concurrent host reads would throttle the HBM gather).
   if (c->refill_pending) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
-  {
-    massive_ctx::Range tr(c, s, 2);
-    launch_gather(kHbm, s, c->d_hbm_list, &c->d_sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
-  }
+  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &c->d_sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
   CK(hipEventRecord(c->ev_classified, s));
   CK(hipStreamWaitEvent(c->s_miss, c->ev_classified, 0));
-  {
-    massive_ctx::Range tr(c, c->s_miss, 3);
-    if (c->H > 0)
-      launch_gather(kMiss, c->s_miss, c->d_miss_list, &c->d_sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb,
-                    nb[c->K], c->host_blocks);
-  }
+  if (c->H > 0)
+    launch_gather(c, 3, kMiss, c->s_miss, c->d_miss_list, &c->d_sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb,
+                  nb[c->K], c->host_blocks);
   CK(hipEventRecord(c->ev_miss_done, c->s_miss));
   CK(hipStreamWaitEvent(s, c->ev_miss_done, 0));
   CK(hipMemcpyAsync(c->h_sz, c->d_sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, s));
@@ -647,10 +678,8 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     }
     CK(hipEventRecord(c->ev_swap_done, s));
     CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
-    {
-      massive_ctx::Range tr(c, c->s_copy, 5);
-      launch_gather(kRefill, c->s_copy, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, c->rb, kk, c->host_blocks);
-    }
+    launch_gather(c, 5, kRefill, c->s_copy, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, c->rb, kk,
+                  c->host_blocks);
     CK(hipEventRecord(c->ev_refill_done, c->s_copy));
     c->refill_pending = true;
   }

@@ -12,6 +12,15 @@ constexpr int kScanTile = kScanNT * kScanItems;
 
 __device__ __forceinline__ int64_t size_of(const int64_t* p, int64_t c) { return p ? *p : c; }
 
+// Sum of partials[0..b) computed by the whole block (b is at most a few
+// thousand): the exclusive prefix of block b without a separate scan kernel.
+template <int NT>
+__device__ __forceinline__ int32_t preceding_sum(const int32_t* __restrict__ partials, int64_t b, int32_t* lds) {
+  int32_t s = 0;
+  for (int64_t i = threadIdx.x; i < b; i += NT) s += partials[i];
+  return block_sum<NT>(s, lds);
+}
+
 // ---------------------------------------------------------------- seeds
 // F_0 = seeds; pos_of[seed] = its position. Flags out-of-range or repeated
 // seeds in sz->status (the step is then abandoned by every later kernel).
@@ -44,9 +53,10 @@ __global__ void k_seed_undo(const int32_t* __restrict__ seeds, int32_t n0, int32
 // Block b: sum over its tile of min(deg(F[i]), fo); counts go to out[i+1].
 __global__ __launch_bounds__(kScanNT) void k_row_counts(const int64_t* __restrict__ csr_indptr,
                                                         const int32_t* __restrict__ nodes,
-                                                        const StepSizes* sz, int hop, int32_t fo,
+                                                        StepSizes* sz, int hop, int32_t fo,
                                                         int32_t* __restrict__ bptr,
-                                                        int32_t* __restrict__ partials) {
+                                                        int32_t* __restrict__ partials,
+                                                        int32_t* __restrict__ big_rows, int64_t big_min) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   if (sz->status) return;
   const int64_t n = sz->n[hop - 1];
@@ -61,10 +71,18 @@ __global__ __launch_bounds__(kScanNT) void k_row_counts(const int64_t* __restric
       const int32_t c = d < fo ? (int32_t)d : fo;
       bptr[i + 1] = c;
       s += c;
+      if (d > big_min) {
+        const unsigned long long b = atomicAdd((unsigned long long*)&sz->n_big[hop - 1], 1ull);
+        big_rows[b] = (int32_t)i;
+      }
     }
   }
   s = block_sum<kScanNT>(s, lds);
-  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+  if (threadIdx.x == 0) {
+    partials[blockIdx.x] = s;
+    if (s) atomicAdd((unsigned long long*)&sz->e[hop - 1], (unsigned long long)s);
+    if (blockIdx.x == 0) sz->n[hop] = n;  // new nodes are added by k_bits_count
+  }
 }
 
 // Exclusive scan of partials[0..nb) in place (one block). Writes the total
@@ -111,8 +129,9 @@ __global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, in
     v[it] = i < n ? bptr[i + 1] : 0;
     s += v[it];
   }
+  const int32_t before = preceding_sum<kScanNT>(partials, blockIdx.x, lds);
   int32_t tot;
-  int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot) + partials[blockIdx.x];
+  int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot) + before;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     const int64_t i = base + it;
@@ -124,132 +143,107 @@ __global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, in
 
 // --------------------------------------------------------------- sampler
 // One wavefront per frontier node. Rows with d <= fanout are copied. For
-// longer rows the choice is the fanout positions of smallest (key, j):
-//   - d <= 256: lane q draws one Philox block = keys of positions 4q..4q+3;
-//   - longer rows: a threshold pass keeps (in ascending j, in LDS) every
-//     position whose key is below tau, tau picked so that about 2*fanout+16
-//     survive (bisection if fewer than fanout or more than 256 survive);
-// then a 32-step bitwise search over ballots finds the fanout-th smallest
-// key T, ties at T are broken by list order (= ascending j), and the chosen
-// positions are written in ascending j.
+// longer rows the choice is the fanout positions of smallest (key, j),
+// found in two stages:
+//   1. a threshold pass draws every key (lane q of an iteration draws one
+//      Philox block = keys of positions 4q..4q+3) and keeps, in ascending j,
+//      the (key, j) pairs with key < tau; tau is set so that about
+//      fanout + 3*sqrt(fanout) + 3 keys survive, and is bisected if fewer than
+//      fanout or more than the list capacity survive (rare);
+//   2. a bitwise search over ballots finds the fanout-th smallest surviving
+//      key T (it starts below tau's top bit), ties at T are taken in list
+//      order (= ascending j), and the chosen positions are written in
+//      ascending j.
+// The chosen ids not yet in the frontier are marked in the new-node bitmap
+// as they are written. Rows longer than big_min (listed by k_row_counts) get
+// the first waves of the grid, so that the longest rows start first.
 constexpr int kSampleWaves = 4;
-constexpr int kCandCap = 256;
+constexpr int kCandCap = 256;   // candidates per wave (LDS); also the largest fanout
+constexpr int64_t kBigRow = 2048;
 
 struct SampleArgs {
   const int64_t* csr_indptr;
   const int32_t* csr_indices;
   const int32_t* nodes;
-  const StepSizes* sz;
+  StepSizes* sz;
   const int32_t* bptr;
   int32_t* out;
   int32_t hop;  // 1-based
   int32_t fo;
   uint32_t t;
   uint32_t key0, key1;
-  int32_t* err;  // threshold search could not isolate a candidate set
+  double mu32;              // (fo + 3 sqrt(fo) + 3) * 2^32
+  int64_t big_min;          // rows longer than this are listed in big_rows
+  const int32_t* big_rows;  // appended by k_row_counts
+  int64_t row_waves;        // waves [0, row_waves) walk the big list, the rest walk all rows
+  const int32_t* pos_of;    // frontier position of an id, or -1
+  uint32_t* bits;           // new-node bitmap
+  int32_t* err;             // threshold search could not isolate a candidate set
 };
 
-__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) {
-  __shared__ uint64_t cand[kSampleWaves][kCandCap];
-  if (a.sz->status) return;
-  const int lane = lane_id(), wave = wave_id();
-  const int64_t row = (int64_t)blockIdx.x * kSampleWaves + wave;
-  const int64_t n = a.sz->n[a.hop - 1];
-  if (row >= n) return;
-  const int32_t v = a.nodes[row];
-  const int64_t start = a.csr_indptr[v];
-  const int64_t d = a.csr_indptr[v + 1] - start;
-  const int32_t fo = a.fo;
-  int32_t* out = a.out + a.bptr[row];
-  const int32_t* nb = a.csr_indices + start;
-  if (d <= fo) {
-    for (int64_t j = lane; j < d; j += MS_WAVE) out[j] = nb[j];
-    return;
+__device__ __forceinline__ uint64_t first_tau(double mu32, int64_t d) {
+  const double t = mu32 / (double)d + 1.0;
+  return t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t;
+}
+
+// Threshold bookkeeping: returns true when the count is acceptable, else
+// moves tau (bisection once both sides are known).
+struct TauSearch {
+  uint64_t lo = 0, hi = (1ull << 32) + 1, tau;
+  __device__ bool step(int cnt, int fo, int cap, bool* fail) {
+    const uint64_t full = 1ull << 32;
+    if (cnt >= fo && cnt <= cap) return true;
+    if (cnt < fo) {
+      lo = tau;
+      tau = (hi > full) ? (tau * 4 > full ? full : tau * 4) : (lo + hi) / 2;
+    } else {
+      hi = tau;
+      tau = (lo + hi) / 2;
+    }
+    if (hi <= full && hi - lo <= 1) *fail = true;
+    return false;
   }
-  const uint32_t uv = (uint32_t)v, ut = a.t, uk = (uint32_t)a.hop;
-  // list element (lane, s) has list index 4*lane + s
+};
+
+__device__ __forceinline__ void emit_id(int32_t* __restrict__ out, int p, int32_t u, const int32_t* __restrict__ pos_of,
+                                        uint32_t* __restrict__ bits) {
+  out[p] = u;
+  if (pos_of[u] < 0) {
+    const uint32_t bit = 1u << (u & 31);
+    if (!(bits[u >> 5] & bit)) atomicOr(&bits[u >> 5], bit);
+  }
+}
+
+// Selection among cnt <= 256 candidates held in LDS in ascending j
+// (list[i] = key << 32 | j); writes the fo chosen neighbours to out in
+// ascending j. One wavefront; element i sits in slot i / 64 of lane i % 64.
+__device__ __forceinline__ void select_emit(const uint64_t* list, int cnt, int fo, uint64_t tau,
+                                            const int32_t* __restrict__ nb, int32_t* __restrict__ out,
+                                            const int32_t* __restrict__ pos_of, uint32_t* __restrict__ bits) {
+  const int lane = lane_id();
+  const int S = (cnt + MS_WAVE - 1) / MS_WAVE;  // 1..4
   uint32_t key[4], pos[4];
   bool valid[4];
-  if (d <= 4 * MS_WAVE) {
-    const uint4 w = philox4x32_10(make_uint4((uint32_t)lane, uv, ut, uk), a.key0, a.key1);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int64_t j = 4 * lane + s;
-      valid[s] = j < d;
-      key[s] = word_of(w, s);
-      pos[s] = (uint32_t)j;
-    }
-  } else {
-    uint64_t* c = cand[wave];
-    const uint64_t full = 1ull << 32;
-    uint64_t tau = ((uint64_t)(2 * fo + 16) << 32) / (uint64_t)d + 1;
-    if (tau > full) tau = full;
-    uint64_t lo = 0, hi = full + 1;  // known: count(lo) < fo; count(hi) > cap (hi unknown: full+1)
-    int cnt = 0;
-    bool ok = false;
-    for (int iter = 0; iter < 48 && !ok; ++iter) {
-      cnt = 0;
-      for (int64_t q0 = 0; 4 * q0 < d; q0 += MS_WAVE) {
-        const int64_t q = q0 + lane;
-        const uint4 w = philox4x32_10(make_uint4((uint32_t)q, uv, ut, uk), a.key0, a.key1);
-        bool take[4];
-        uint64_t m[4];
-        int mine = 0;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          take[s] = (4 * q + s < d) && ((uint64_t)word_of(w, s) < tau);
-          m[s] = ballot(take[s]);
-        }
-        int below = lanes_below(m[0]) + lanes_below(m[1]) + lanes_below(m[2]) + lanes_below(m[3]);
-        const int total = __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          if (take[s]) {
-            const int p = cnt + below + mine;
-            if (p < kCandCap) c[p] = ((uint64_t)word_of(w, s) << 32) | (uint32_t)(4 * q + s);
-            ++mine;
-          }
-        }
-        cnt += total;
-      }
-      if (cnt < fo) {
-        lo = tau;
-        tau = (hi > full) ? (tau * 4 > full ? full : tau * 4) : (lo + hi) / 2;
-      } else if (cnt > kCandCap) {
-        hi = tau;
-        tau = (lo + hi) / 2;
-      } else {
-        ok = true;
-      }
-      if (!ok && hi <= full && hi - lo <= 1) break;
-    }
-    if (!ok) {
-      if (lane == 0) atomicOr(a.err, 1);
-      return;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int idx = 4 * lane + s;
-      valid[s] = idx < cnt;
-      const uint64_t e = valid[s] ? c[idx] : 0ull;
-      key[s] = (uint32_t)(e >> 32);
-      pos[s] = (uint32_t)e;
-    }
+  for (int s = 0; s < 4; ++s) {
+    const int idx = s * MS_WAVE + lane;
+    valid[s] = s < S && idx < cnt;
+    const uint64_t e = valid[s] ? list[idx] : 0ull;
+    key[s] = (uint32_t)(e >> 32);
+    pos[s] = (uint32_t)e;
   }
-  // T = largest x with count(key < x) < fo, i.e. the fo-th smallest key
+  // T = largest x with count(key < x) < fo; every key is below tau
   uint32_t T = 0;
-  for (int b = 31; b >= 0; --b) {
+  const uint64_t tm1 = tau - 1;
+  const int top = tm1 == 0 ? 0 : 63 - __clzll(tm1);
+  for (int b = top; b >= 0; --b) {
     const uint32_t trial = T | (1u << b);
-    int c = 0;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) c += __popcll(ballot(valid[s] && key[s] < trial));
+    int c = __popcll(ballot(valid[0] && key[0] < trial));
+    for (int s = 1; s < S; ++s) c += __popcll(ballot(valid[s] && key[s] < trial));
     if (c < fo) T = trial;
   }
-  uint64_t lt[4], eq[4];
   int n_lt = 0;
+  uint64_t lt[4], eq[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     lt[s] = ballot(valid[s] && key[s] < T);
@@ -257,47 +251,96 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) 
     n_lt += __popcll(lt[s]);
   }
   const int need = fo - n_lt;
-  // rank among ties in list order, then the selection mask
-  int eq_below = lanes_below(eq[0]) + lanes_below(eq[1]) + lanes_below(eq[2]) + lanes_below(eq[3]);
-  bool sel[4];
+  int eq_before = 0;  // ties in earlier slots (all lanes)
+  int p_before = 0;   // selected in earlier slots
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    const bool is_eq = (eq[s] >> lane) & 1ull;
-    sel[s] = ((lt[s] >> lane) & 1ull) || (is_eq && eq_below < need);
-    if (is_eq) ++eq_below;
+    const bool is_lt = (lt[s] >> lane) & 1ull, is_eq = (eq[s] >> lane) & 1ull;
+    const bool sel = is_lt || (is_eq && eq_before + lanes_below(eq[s]) < need);
+    const uint64_t sm = ballot(sel);
+    if (sel) emit_id(out, p_before + lanes_below(sm), nb[pos[s]], pos_of, bits);
+    p_before += __popcll(sm);
+    eq_before += __popcll(eq[s]);
   }
-  uint64_t sm[4];
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) {
+  __shared__ uint64_t cand[kSampleWaves][kCandCap];
+  if (a.sz->status) return;
+  const int lane = lane_id(), wave = wave_id();
+  const int64_t w = (int64_t)blockIdx.x * kSampleWaves + wave;
+  int64_t row;
+  if (w < a.row_waves) {
+    if (w >= a.sz->n_big[a.hop - 1]) return;
+    row = a.big_rows[w];
+  } else {
+    row = w - a.row_waves;
+    if (row >= a.sz->n[a.hop - 1]) return;
+  }
+  const int32_t v = a.nodes[row];
+  const int64_t start = a.csr_indptr[v];
+  const int64_t d = a.csr_indptr[v + 1] - start;
+  if (w >= a.row_waves && d > a.big_min) return;  // taken by a wave of the big list
+  const int32_t fo = a.fo;
+  int32_t* out = a.out + a.bptr[row];
+  const int32_t* nb = a.csr_indices + start;
+  if (d <= fo) {
+    for (int64_t j = lane; j < d; j += MS_WAVE) emit_id(out, (int)j, nb[j], a.pos_of, a.bits);
+    return;
+  }
+  uint64_t* c = cand[wave];
+  TauSearch ts;
+  ts.tau = first_tau(a.mu32, d);
+  int cnt = 0;
+  bool fail = false;
+  const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
+  for (int iter = 0; iter < 48 && !fail; ++iter) {
+    cnt = 0;
+    const uint32_t tm1 = (uint32_t)(ts.tau - 1);  // key < tau  <=>  key <= tau - 1
+    for (uint32_t q0 = 0; 4 * q0 < d32; q0 += MS_WAVE) {
+      const uint32_t q = q0 + lane;
+      const uint4 wv = philox4x32_10(make_uint4(q, (uint32_t)v, a.t, (uint32_t)a.hop), a.key0, a.key1);
+      bool take[4];
+      if (4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
 #pragma unroll
-  for (int s = 0; s < 4; ++s) sm[s] = ballot(sel[s]);
-  int p = lanes_below(sm[0]) + lanes_below(sm[1]) + lanes_below(sm[2]) + lanes_below(sm[3]);
+        for (int s = 0; s < 4; ++s) take[s] = word_of(wv, s) <= tm1;
+      } else {
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    if (sel[s]) {
-      out[p] = nb[pos[s]];
-      ++p;
+        for (int s = 0; s < 4; ++s) take[s] = (4 * q + s < d32) && word_of(wv, s) <= tm1;
+      }
+      if (!ballot(take[0] || take[1] || take[2] || take[3])) continue;  // usual case for long rows
+      uint64_t m[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) m[s] = ballot(take[s]);
+      int p = cnt + lanes_below(m[0]) + lanes_below(m[1]) + lanes_below(m[2]) + lanes_below(m[3]);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        if (take[s]) {
+          if (p < kCandCap) c[p] = ((uint64_t)word_of(wv, s) << 32) | (4 * q + s);
+          ++p;
+        }
+      cnt += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
     }
+    if (ts.step(cnt, fo, kCandCap, &fail)) break;
   }
+  if (fail) {
+    if (lane == 0) atomicOr(a.err, 4);
+    return;
+  }
+  wave_lds_sync();
+  select_emit(c, cnt, fo, ts.tau, nb, out, a.pos_of, a.bits);
 }
 
 // ------------------------------------------------------------ dedup/relabel
-// Mark every sampled id not yet in the frontier in a bitmap over [0, L+H).
-__global__ void k_mark_new(const int32_t* __restrict__ ids, const StepSizes* sz, int hop,
-                           const int32_t* __restrict__ pos_of, uint32_t* __restrict__ bits) {
-  if (sz->status) return;
-  const int64_t e = sz->e[hop - 1];
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < e;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t u = ids[i];
-    if (pos_of[u] < 0) {
-      const uint32_t bit = 1u << (u & 31);
-      if (!(bits[u >> 5] & bit)) atomicOr(&bits[u >> 5], bit);
-    }
-  }
-}
-
 // Per-block popcount of the bitmap tile.
 __global__ __launch_bounds__(kScanNT) void k_bits_count(const uint32_t* __restrict__ bits, int64_t W,
-                                                        const StepSizes* sz,
+                                                        StepSizes* sz, int hop,
                                                         int32_t* __restrict__ partials) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   if (sz->status) return;
@@ -311,7 +354,10 @@ __global__ __launch_bounds__(kScanNT) void k_bits_count(const uint32_t* __restri
       if (base + it < W) s += __popc(bits[base + it]);
   }
   s = block_sum<kScanNT>(s, lds);
-  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+  if (threadIdx.x == 0) {
+    partials[blockIdx.x] = s;
+    if (s) atomicAdd((unsigned long long*)&sz->n[hop], (unsigned long long)s);
+  }
 }
 
 // New nodes in ascending id: F[n_{k-1} + rank] = u, pos_of[u] = that
@@ -331,9 +377,9 @@ __global__ __launch_bounds__(kScanNT) void k_bits_emit(uint32_t* __restrict__ bi
     w[it] = base + it < W ? bits[base + it] : 0u;
     s += __popc(w[it]);
   }
+  const int32_t before = preceding_sum<kScanNT>(partials, blockIdx.x, lds);
   int32_t tot;
-  int64_t off = (int64_t)block_exclusive_scan<kScanNT>(s, lds, &tot) + partials[blockIdx.x] +
-                sz->n[hop - 1];
+  int64_t off = (int64_t)block_exclusive_scan<kScanNT>(s, lds, &tot) + before + sz->n[hop - 1];
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     uint32_t x = w[it];
