@@ -79,7 +79,7 @@ def main():
     torch.cuda.synchronize()
     init_s = time.time() - t0
     log("massive_init %.2fs: cap=%d alpha=%.6g" % (init_s, gm.cap, gm.alpha))
-    bb = gm.alloc_batch(w.batch)
+    bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
     total = args.warmup + args.steps
     seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
     torch.cuda.synchronize()
@@ -93,35 +93,43 @@ def main():
         log("copy probe: 256 MiB device-to-device copy done")
         del a, b
 
-    first_steps = []  # digests of the first steps, checked against the oracle below
-    for t in range(args.warmup):
-        r = gm.sample(seeds_dev[t], bb)
-        if args.log_steps:
-            log("step %d local %d hits %d misses %d rows %d" % (t, r.local, r.hits, r.misses, r.n[-1]))
-        if t < 2:
-            nK = r.n[-1]
-            first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
-                                bb.feat[:nK].cpu().numpy().copy()))
-        gm.evict_step()
+    first_steps = []  # the first steps' outputs, checked against the oracle below
+
+    def run(t0, t1, stats):
+        """Steps t0..t1-1 with look-ahead: step t+1 is enqueued (after step t's
+        round) before step t is waited for, so its sampling overlaps step t's
+        host-link reads."""
+        prev = None
+        for t in range(t0, t1 + 1):
+            if t < t1:
+                gm.sample_async(seeds_dev[t], bbs[t % 2])
+                gm.evict_step(wait=False)
+            if prev is not None:
+                r = gm.wait(bbs[prev % 2])
+                stats.append((r.local, r.hits, r.misses, r.n[-1]))
+                if prev < 2 and len(first_steps) == prev:
+                    bb = bbs[prev % 2]
+                    nK = r.n[-1]
+                    first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
+                                        bb.feat[:nK].cpu().numpy().copy()))
+                if args.log_steps:
+                    log("step %d local %d hits %d misses %d rows %d" % (prev, r.local, r.hits, r.misses, r.n[-1]))
+            prev = t
+
+    run(0, args.warmup, [])
     log("warmup %d steps done" % args.warmup)
+    r0, e0 = gm.counters()
 
     gm.set_timing(True)
     stats = []
-    rounds = 0
-    evicted = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for t in range(args.warmup, total):
-        r = gm.sample(seeds_dev[t], bb)
-        k = gm.evict_step()
-        stats.append((r.local, r.hits, r.misses, r.n[-1]))
-        if args.log_steps:
-            log("step %d local %d hits %d misses %d rows %d" % (t, r.local, r.hits, r.misses, r.n[-1]))
-        rounds += k > 0
-        evicted += k
+    run(args.warmup, total, stats)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     tim = gm.timing()
+    r1, e1 = gm.counters()
+    rounds, evicted = r1 - r0, e1 - e0
     K = args.steps
     mbps = K / elapsed
     log("timed %d steps in %.3fs: %.1f minibatches/s, %d rounds, %d evicted" % (K, elapsed, mbps, rounds, evicted))
@@ -166,7 +174,7 @@ def main():
                    "L": g.L, "H": g.H, "csr_entries": g.nnz, "batch": w.batch, "fanout": list(w.fanout),
                    "row_bytes": rb, "buffer_pct": w.buffer_pct, "gamma": w.gamma, "delta": w.delta,
                    "cap": gm.cap, "steps_timed": [args.warmup, total - 1], "eviction_rounds": rounds,
-                   "evicted_rows": evicted, "parallelism": "one partition on one GPU"},
+                   "evicted_rows": evicted, "lookahead": 1, "parallelism": "one partition on one GPU"},
         "gather_GBps": round(g_gbps, 1),
         "gather_frac_hbm": round(g_gbps / HBM_PEAK_GBPS, 4),
         "hit_rate": round(hit_rate, 4),

@@ -119,20 +119,40 @@ typedef struct {
  * n_seeds device seeds (distinct local ids), classifies every frontier node
  * against the buffer, updates the scores and gathers all feature rows (HBM
  * rows from the local slab and the buffer, misses from halo_store). Returns
- * after the batch is complete on the device; then t advances by one.
+ * after the batch is complete on the device (massive_sample_async followed by
+ * massive_batch_wait); t advances by one.
  * MASSIVE_ESTATE if the previous step's massive_evict_step was not called.
  * MASSIVE_EINVAL (no state change) if a seed is out of [0, L) or repeated. */
 int massive_sample(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
 
+/* The asynchronous form of massive_sample, for look-ahead (Algorithm 1
+ * prepares the next minibatch while the current one is consumed): enqueues
+ * the step and returns at once. The batch's buffers must not be read or
+ * reused, and its sizes are not written, until massive_batch_wait returns for
+ * it. At most two batches are in flight: the next step can be enqueued (after
+ * its predecessor's massive_evict_step) while the previous one still reads
+ * misses over the host link. Argument errors are returned here; seed errors
+ * are returned by massive_batch_wait (if a later step was already issued the
+ * context then refuses further work with MASSIVE_ESTATE). */
+int massive_sample_async(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
+
+/* Waits for the batch enqueued with io and writes its sizes and counters. */
+int massive_batch_wait(massive_ctx* ctx, massive_batch* io);
+
 /* The eviction round owed by the step just sampled; must be called once after
- * every massive_sample. Runs the round iff that step t has t > 0 and
- * t mod delta == 0, else sets *k_out = 0. Optional device outputs, each with
- * room for cap entries: evicted halo ids, the slots they held (ascending),
- * and their replacements. The replacement rows are copied from halo_store on
- * a side stream that overlaps the next step's sampling; the next step's
- * gather waits for them. */
+ * every massive_sample / massive_sample_async. Runs the round iff that step t
+ * has t > 0 and t mod delta == 0. The round is decided on the device: with
+ * k_out == NULL the call only enqueues it; otherwise it waits and writes k'
+ * (0 when no round is due). Optional device outputs, each with room for cap
+ * entries: evicted halo ids, the slots they held (ascending), and their
+ * replacements (entries [0, k')). The replacement rows are copied from
+ * halo_store on a copy stream; until they have landed, the next steps read
+ * hits on those slots from halo_store (the same bytes). */
 int massive_evict_step(massive_ctx* ctx, int32_t* evicted, int32_t* slots, int32_t* replaced,
                        int64_t* k_out);
+
+/* Totals since init: rounds that evicted at least one slot, slots evicted. */
+int massive_get_counters(massive_ctx* ctx, int64_t* rounds, int64_t* evicted);
 
 /* Host copies of the prefetcher state (each pointer may be NULL):
  * slot_id[cap] halo id per slot, S_E[cap], S_A[H], steps sampled so far. */

@@ -31,7 +31,8 @@ __device__ __forceinline__ int32_t hash_find(const uint64_t* __restrict__ tab, u
 }
 
 __global__ void k_hash_insert(uint64_t* __restrict__ tab, uint32_t mask, const int32_t* __restrict__ slot_id,
-                              int64_t cap) {
+                              int64_t cap, const int64_t* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < cap;
        s += (int64_t)gridDim.x * blockDim.x) {
     const int32_t h = slot_id[s];
@@ -68,6 +69,8 @@ struct ClassifyArgs {
   uint8_t* mask;
   int2* hbm_list;
   int2* miss_list;
+  const int32_t* slot_round;  // round that last refilled each slot
+  int32_t pend_round;         // refill of this round may still be in flight (-1: none)
 };
 
 constexpr int kClsNT = 256;
@@ -77,7 +80,7 @@ constexpr int kClsItems = 8;  // rows per thread: one block classifies 2048 rows
 // base per list with a single atomic, and places rows with wave ballots.
 __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   constexpr int NW = kClsNT / MS_WAVE;
-  __shared__ int32_t wc[NW][3];          // per-wave counts: hbm, miss, local
+  __shared__ int32_t wc[NW][4];          // per-wave counts: hbm list, host list, local, pending hits
   __shared__ unsigned long long base[2];
   if (a.sz->status) return;
   const int64_t n = a.sz->n[a.K];
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   for (int64_t b0 = (int64_t)blockIdx.x * tile; b0 < n; b0 += (int64_t)gridDim.x * tile) {
     int cls[kClsItems];
     int32_t src[kClsItems];
-    int ch = 0, cm = 0, cl = 0;
+    int ch = 0, cm = 0, cl = 0, cp = 0;  // hbm list, host list, local, pending hits
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
       // wave w of item it covers rows b0 + it*256 + w*64 + lane
@@ -106,36 +109,45 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
             cls[it] = 1;
             src[it] = a.L + slot;
             a.hitcnt[slot] += 1;
+            // a hit on a slot whose refill may not have landed reads the same
+            // row from the host store
+            if (a.pend_round >= 0 && a.slot_round[slot] == a.pend_round) {
+              cls[it] = 3;
+              src[it] = h;
+            }
           } else {
             cls[it] = 2;
             src[it] = h;
             atomicAdd(&a.S_A[h], 1.0f);
           }
         }
-        a.mask[i] = (uint8_t)cls[it];
+        a.mask[i] = (uint8_t)(cls[it] == 3 ? 1 : cls[it]);
       }
       ch += __popcll(ballot(cls[it] == 0 || cls[it] == 1));
-      cm += __popcll(ballot(cls[it] == 2));
+      cm += __popcll(ballot(cls[it] >= 2));
       cl += __popcll(ballot(cls[it] == 0));
+      cp += __popcll(ballot(cls[it] == 3));
     }
     if (lane == 0) {
       wc[wave][0] = ch;
       wc[wave][1] = cm;
       wc[wave][2] = cl;
+      wc[wave][3] = cp;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-      int th = 0, tm = 0, tl = 0;
+      int th = 0, tm = 0, tl = 0, tp = 0;
       for (int w = 0; w < NW; ++w) {
         th += wc[w][0];
         tm += wc[w][1];
         tl += wc[w][2];
+        tp += wc[w][3];
       }
       base[0] = th ? atomicAdd((unsigned long long*)&a.sz->n_hbm, (unsigned long long)th) : 0ull;
       base[1] = tm ? atomicAdd((unsigned long long*)&a.sz->n_miss, (unsigned long long)tm) : 0ull;
       if (tl) atomicAdd((unsigned long long*)&a.sz->local, (unsigned long long)tl);
-      if (th - tl) atomicAdd((unsigned long long*)&a.sz->hits, (unsigned long long)(th - tl));
-      if (tm) atomicAdd((unsigned long long*)&a.sz->misses, (unsigned long long)tm);
+      if (th - tl + tp) atomicAdd((unsigned long long*)&a.sz->hits, (unsigned long long)(th - tl + tp));
+      if (tm - tp) atomicAdd((unsigned long long*)&a.sz->misses, (unsigned long long)(tm - tp));
     }
     __syncthreads();
     // this wave's offset inside the block's share of each list
@@ -148,9 +160,9 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
     for (int it = 0; it < kClsItems; ++it) {
       const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
       const uint64_t mh = ballot(cls[it] == 0 || cls[it] == 1);
-      const uint64_t mm = ballot(cls[it] == 2);
+      const uint64_t mm = ballot(cls[it] >= 2);
       if (cls[it] == 0 || cls[it] == 1) a.hbm_list[oh + lanes_below(mh)] = make_int2((int32_t)i, src[it]);
-      else if (cls[it] == 2) a.miss_list[om + lanes_below(mm)] = make_int2((int32_t)i, src[it]);
+      else if (cls[it] >= 2) a.miss_list[om + lanes_below(mm)] = make_int2((int32_t)i, src[it]);
       oh += __popcll(mh);
       om += __popcll(mm);
     }
@@ -243,7 +255,7 @@ __global__ void k_materialize(float* __restrict__ S_E, int32_t* __restrict__ hit
 // ------------------------------------------------- ordered flag compaction
 // E = [s : S_E[s] < alpha] in ascending s, as count / scan / emit.
 __global__ __launch_bounds__(kScanNT) void k_evict_count(const float* __restrict__ S_E, int64_t cap, float alpha,
-                                                         int32_t* __restrict__ partials) {
+                                                         int32_t* __restrict__ partials, int64_t* __restrict__ total) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
   int32_t s = 0;
@@ -253,7 +265,10 @@ __global__ __launch_bounds__(kScanNT) void k_evict_count(const float* __restrict
     s += (i < cap && S_E[i] < alpha) ? 1 : 0;
   }
   s = block_sum<kScanNT>(s, lds);
-  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+  if (threadIdx.x == 0) {
+    partials[blockIdx.x] = s;
+    if (s) atomicAdd((unsigned long long*)total, (unsigned long long)s);
+  }
 }
 
 __global__ __launch_bounds__(kScanNT) void k_evict_emit(const float* __restrict__ S_E, int64_t cap, float alpha,
@@ -269,8 +284,9 @@ __global__ __launch_bounds__(kScanNT) void k_evict_emit(const float* __restrict_
     f[it] = i < cap && S_E[i] < alpha;
     s += f[it];
   }
+  const int32_t before = preceding_sum<kScanNT>(partials, blockIdx.x, lds);
   int32_t tot;
-  int32_t o = block_exclusive_scan<kScanNT>(s, lds, &tot) + partials[blockIdx.x];
+  int32_t o = block_exclusive_scan<kScanNT>(s, lds, &tot) + before;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it)
     if (f[it]) E[o++] = (int32_t)(base + it);
@@ -287,6 +303,28 @@ __global__ __launch_bounds__(256) void k_count_candidates(const float* __restric
   if (threadIdx.x == 0 && c) atomicAdd((unsigned long long*)out, (unsigned long long)c);
 }
 
+// k' = min(|E|, |C|) on the device; sets the select and the E narrowing up.
+__global__ void k_round_setup(RoundState* __restrict__ rs, Counters* __restrict__ ctr) {
+  const int64_t k = rs->nE < rs->nC ? rs->nE : rs->nC;
+  rs->k = k;
+  rs->need = k;
+  rs->prefix = 0;
+  rs->pmask = 0;
+  rs->nE_sel = k < rs->nE ? rs->nE : 0;
+  rs->k_sel = k < rs->nE ? k : 0;
+  if (k > 0) {
+    ctr->rounds += 1;
+    ctr->evicted += k;
+  }
+}
+
+template <typename T>
+__global__ void k_fill_gated(T* __restrict__ p, int64_t n, T v, const int64_t* __restrict__ gate) {
+  if (*gate == 0) return;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
 // ------------------------------------------------------ replacement select
 // Candidate key: bitwise NOT of the fp32 bits of S_A >= 0, so ascending key
 // is descending S_A. Radix select, 8 bits per pass from the top, finds the
@@ -297,6 +335,7 @@ __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S
                                                      const RoundState* __restrict__ rs, int shift,
                                                      uint32_t* __restrict__ ghist) {
   __shared__ uint32_t hist[256];
+  if (rs->k == 0) return;
   hist[threadIdx.x] = 0;
   __syncthreads();
   const uint32_t prefix = rs->prefix, pmask = rs->pmask;
@@ -312,10 +351,11 @@ __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S
 }
 
 __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs, uint32_t* __restrict__ ghist,
-                                                     int shift) {
+                                                     int shift, int32_t* __restrict__ bad) {
   __shared__ int64_t lds[256 / MS_WAVE + 1];
   __shared__ int32_t pick;
   __shared__ int64_t before;
+  if (rs->k == 0) return;
   if (threadIdx.x == 0) {
     pick = -1;
     before = 0;
@@ -333,7 +373,7 @@ __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs
   ghist[threadIdx.x] = 0;
   if (threadIdx.x == 0) {
     if (pick < 0) {  // fewer candidates than asked for: never expected
-      rs->bad |= 2;
+      atomicOr(bad, 2);
       rs->need = 0;
     } else {
       rs->need = need - before;
@@ -347,16 +387,17 @@ __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs
 // the first `need` with key == T go straight to R[n_lt + ...].
 __global__ __launch_bounds__(kScanNT) void k_rank_count(const float* __restrict__ S_A,
                                                         const int32_t* __restrict__ h_of_rank, int64_t H,
-                                                        const RoundState* __restrict__ rs,
+                                                        RoundState* __restrict__ rs,
                                                         int32_t* __restrict__ p_lt, int32_t* __restrict__ p_eq) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   const uint32_t T = rs->prefix;
+  const bool on = rs->k > 0;
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
   int32_t clt = 0, ceq = 0;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     const int64_t r = base + (int64_t)it * kScanNT + threadIdx.x;
-    if (r < H) {
+    if (on && r < H) {
       const float a = S_A[h_of_rank[r]];
       if (a >= 0.0f) {
         const uint32_t k = cand_key(a);
@@ -370,6 +411,8 @@ __global__ __launch_bounds__(kScanNT) void k_rank_count(const float* __restrict_
   if (threadIdx.x == 0) {
     p_lt[blockIdx.x] = clt;
     p_eq[blockIdx.x] = ceq;
+    if (clt) atomicAdd((unsigned long long*)&rs->n_lt, (unsigned long long)clt);
+    if (ceq) atomicAdd((unsigned long long*)&rs->n_eq, (unsigned long long)ceq);
   }
 }
 
@@ -381,6 +424,7 @@ __global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__
                                                        uint32_t* __restrict__ keys, int32_t* __restrict__ vals,
                                                        int32_t* __restrict__ R) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  if (rs->k == 0) return;
   const uint32_t T = rs->prefix;
   const int64_t need = rs->need, n_lt = rs->k - rs->need;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
@@ -404,9 +448,11 @@ __global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__
     clt += lt[it];
     ceq += eq[it];
   }
+  const int32_t blt = preceding_sum<kScanNT>(p_lt, blockIdx.x, lds);
+  const int32_t beq = preceding_sum<kScanNT>(p_eq, blockIdx.x, lds);
   int32_t tlt, teq;
-  int64_t olt = (int64_t)block_exclusive_scan<kScanNT>(clt, lds, &tlt) + p_lt[blockIdx.x];
-  int64_t oeq = (int64_t)block_exclusive_scan<kScanNT>(ceq, lds, &teq) + p_eq[blockIdx.x];
+  int64_t olt = (int64_t)block_exclusive_scan<kScanNT>(clt, lds, &tlt) + blt;
+  int64_t oeq = (int64_t)block_exclusive_scan<kScanNT>(ceq, lds, &teq) + beq;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     if (lt[it]) {
@@ -603,7 +649,8 @@ __global__ void k_esel_keys_slot(const int32_t* __restrict__ vals, const int64_t
 __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict__ R, const int64_t* __restrict__ k_ptr,
                        int32_t L, int64_t cap, int32_t H, int32_t* __restrict__ slot_id, float* __restrict__ S_E,
                        float* __restrict__ S_A, int32_t* __restrict__ out_ev, int32_t* __restrict__ out_slot,
-                       int32_t* __restrict__ out_rep, int2* __restrict__ fill, int32_t* __restrict__ bad) {
+                       int32_t* __restrict__ out_rep, int2* __restrict__ fill, int32_t* __restrict__ bad,
+                       int32_t* __restrict__ slot_round, int32_t round_id) {
   const int64_t k = *k_ptr;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < k; i += (int64_t)gridDim.x * blockDim.x) {
     const int32_t s = E[i], r = R[i];
@@ -618,6 +665,7 @@ __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict_
     S_E[s] = sa;
     S_A[r] = -1.0f;
     slot_id[s] = r;
+    slot_round[s] = round_id;
     if (out_ev) out_ev[i] = e;
     if (out_slot) out_slot[i] = s;
     if (out_rep) out_rep[i] = r;

@@ -106,8 +106,14 @@ struct RoundState {
   int64_t need;            // ties at the threshold still to take
   uint32_t prefix, pmask;  // radix-select prefix of the threshold key
   int64_t n_lt, n_eq;      // candidates strictly before / equal to the threshold
-  int64_t ksel;            // for E selection when k' < |E|
-  int32_t bad;             // inconsistent select / swap indices (never expected)
+  int64_t nE_sel, k_sel;   // |E| and k' when k' < |E| (E must be narrowed), else 0
+};
+
+// Totals over the context's life (device side).
+struct Counters {
+  int64_t rounds;          // rounds that evicted at least one slot
+  int64_t evicted;         // slots evicted (= rows refilled)
+  int32_t bad;             // some round produced inconsistent indices (never expected)
   int32_t pad;
 };
 

@@ -62,8 +62,11 @@ struct massive_ctx {
   int64_t big_min = ms::kBigRow;        // rows longer than this use the 16-wave kernel
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
-  hipEvent_t ev_classified = nullptr, ev_miss_done = nullptr, ev_swap_done = nullptr, ev_refill_done = nullptr;
-  bool refill_pending = false;
+  // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
+  hipEvent_t ev_hbm_done[2] = {}, ev_batch_done[2] = {};
+  hipEvent_t ev_swap_done = nullptr, ev_refill_done = nullptr;
+  bool refill_inflight = false;  // the last round's refill may not have landed
+  int32_t round_id = 0;          // rounds that swapped at least one slot, as stamped in slot_round
   // device memory
   int64_t* d_indptr = nullptr;
   int32_t* d_indices = nullptr;
@@ -78,14 +81,18 @@ struct massive_ctx {
   uint64_t* d_tab = nullptr;
   int32_t* d_pos_of = nullptr;
   uint32_t* d_bits = nullptr;
-  ms::StepSizes* d_sz = nullptr;
-  ms::StepSizes* h_sz = nullptr;      // pinned mailbox
+  ms::StepSizes* d_sz = nullptr;      // [2], by step parity
+  ms::StepSizes* h_sz = nullptr;      // [2] pinned mailboxes
+  int32_t* h_bad = nullptr;           // [2] pinned: eviction-round consistency flag
   ms::RoundState* d_rs = nullptr;
   ms::RoundState* h_rs = nullptr;     // pinned mailbox
+  ms::Counters* d_ctr = nullptr;
+  ms::Counters* h_ctr = nullptr;      // pinned
+  int32_t* d_slot_round = nullptr;    // [cap]
   int32_t* d_part = nullptr;
   int32_t* d_part2 = nullptr;
   int2* d_hbm_list = nullptr;
-  int2* d_miss_list = nullptr;
+  int2* d_miss_list[2] = {};          // by step parity (read by the side stream)
   int32_t* d_E = nullptr;
   int32_t* d_R = nullptr;
   int2* d_fill = nullptr;
@@ -100,6 +107,12 @@ struct massive_ctx {
   int64_t mat_t = 0;    // S_E materialised through this many steps
   bool pending_round = false;
   bool broken = false;
+  struct InFlight {
+    massive_batch* io = nullptr;
+    int64_t step = -1;
+    const int32_t* seeds = nullptr;
+    int32_t n0 = 0;
+  } infl[2];
   // timing
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
@@ -273,13 +286,17 @@ void free_ctx(massive_ctx* c) {
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
-                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list, c->d_E, c->d_R, c->d_fill,
+                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_E, c->d_R,
+                 c->d_fill, c->d_ctr, c->d_slot_round,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   if (c->h_sz) (void)hipHostFree(c->h_sz);
   if (c->h_rs) (void)hipHostFree(c->h_rs);
-  for (hipEvent_t e : {c->ev_classified, c->ev_miss_done, c->ev_swap_done, c->ev_refill_done})
+  if (c->h_bad) (void)hipHostFree(c->h_bad);
+  if (c->h_ctr) (void)hipHostFree(c->h_ctr);
+  for (hipEvent_t e : {c->ev_hbm_done[0], c->ev_hbm_done[1], c->ev_batch_done[0], c->ev_batch_done[1],
+                       c->ev_swap_done, c->ev_refill_done})
     if (e) (void)hipEventDestroy(e);
   for (auto& r : c->pending) {
     (void)hipEventDestroy(r.a);
@@ -327,7 +344,8 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
-  for (hipEvent_t* e : {&c->ev_classified, &c->ev_miss_done, &c->ev_swap_done, &c->ev_refill_done})
+  for (hipEvent_t* e : {&c->ev_hbm_done[0], &c->ev_hbm_done[1], &c->ev_batch_done[0], &c->ev_batch_done[1],
+                        &c->ev_swap_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
 
   // the pinned store must be mapped into the device address space
@@ -355,12 +373,15 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_pos_of, R * 4);
   CKA(c->d_big, R * 4);
   CKA(c->d_bits, (c->W + 4) * 4);
-  CKA(c->d_sz, sizeof(ms::StepSizes));
+  CKA(c->d_sz, 2 * sizeof(ms::StepSizes));
   CKA(c->d_rs, sizeof(ms::RoundState));
+  CKA(c->d_ctr, sizeof(ms::Counters));
+  CKA(c->d_slot_round, cap * 4);
   CKA(c->d_part, c->pmax * 4);
   CKA(c->d_part2, c->pmax * 4);
   CKA(c->d_hbm_list, R * 8);
-  CKA(c->d_miss_list, R * 8);
+  CKA(c->d_miss_list[0], R * 8);
+  CKA(c->d_miss_list[1], R * 8);
   CKA(c->d_E, cap * 4);
   CKA(c->d_R, cap * 4);
   CKA(c->d_fill, cap * 8);
@@ -370,8 +391,10 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_v1, c->sort_cap * 4);
   CKA(c->d_hist, 256 * cdiv(c->sort_cap, ms::kSortTile) * 4);
   CKA(c->d_ghist, 256 * 4);
-  if (hipHostMalloc((void**)&c->h_sz, sizeof(ms::StepSizes), hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_rs, sizeof(ms::RoundState), hipHostMallocDefault) != hipSuccess)
+  if (hipHostMalloc((void**)&c->h_sz, 2 * sizeof(ms::StepSizes), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_rs, sizeof(ms::RoundState), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_bad, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_ctr, sizeof(ms::Counters), hipHostMallocDefault) != hipSuccess)
     return c->fail(MASSIVE_ENOMEM, "hipHostMalloc of the size mailboxes failed");
 
   hipStream_t s = c->s_main;
@@ -379,18 +402,20 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (c->nnz) CK(hipMemcpyAsync(c->d_indices, a->indices, c->nnz * 4, hipMemcpyHostToDevice, s));
   if (c->L) CK(hipMemcpyAsync(c->d_slab, a->local_feat, (int64_t)c->L * rb, hipMemcpyHostToDevice, s));
   {
-    CK(hipMemsetAsync(&c->d_rs->bad, 0, 4, s));
+    CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
     ms::k_validate_csr<<<grid_for(std::max(R, c->nnz), 256, 8192), 256, 0, s>>>(c->d_indptr, R, c->d_indices, c->nnz,
-                                                                                &c->d_rs->bad);
-    CK(hipMemcpyAsync(&c->h_rs->bad, &c->d_rs->bad, 4, hipMemcpyDeviceToHost, s));
+                                                                                &c->d_ctr->bad);
+    CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
     CK(hipStreamSynchronize(s));
-    if (c->h_rs->bad)
-      return c->fail(MASSIVE_EINVAL, (c->h_rs->bad & 2) ? "indices has ids outside [0, L+H)"
-                                                         : "indptr is not non-decreasing");
+    if (c->h_ctr->bad)
+      return c->fail(MASSIVE_EINVAL, (c->h_ctr->bad & 2) ? "indices has ids outside [0, L+H)"
+                                                          : "indptr is not non-decreasing");
   }
   CK(hipMemsetAsync(c->d_pos_of, 0xFF, R * 4, s));
   CK(hipMemsetAsync(c->d_bits, 0, (c->W + 4) * 4, s));
   CK(hipMemsetAsync(c->d_ghist, 0, 256 * 4, s));
+  CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
+  CK(hipMemsetAsync(c->d_slot_round, 0xFF, cap * 4, s));
 
   if (H > 0) {
     // halo rank: (degree desc, global id asc) by two stable radix sorts
@@ -414,14 +439,20 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (cap > 0) {
     ms::k_init_buffer<<<grid_for(cap, 256), 256, 0, s>>>(c->d_h_of_rank, cap, c->L, c->d_slot_id, c->d_S_E,
                                                          c->d_hitcnt, c->d_S_A, c->d_fill);
-    ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap);
+    ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, nullptr);
     // the cap best-ranked rows arrive over the host link
     c->h_rs->k = cap;
     CK(hipMemcpyAsync(&c->d_rs->k, &c->h_rs->k, 8, hipMemcpyHostToDevice, s));
     launch_gather(c, 5, kRefill, s, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, rb, cap, c->host_blocks);
   }
+  // the step-parity events start out complete
+  for (int i = 0; i < 2; ++i) {
+    CK(hipEventRecord(c->ev_hbm_done[i], s));
+    CK(hipEventRecord(c->ev_batch_done[i], c->s_miss));
+  }
   CK(hipGetLastError());
   CK(hipStreamSynchronize(s));
+  CK(hipStreamSynchronize(c->s_miss));
   return MASSIVE_OK;
 }
 
@@ -476,12 +507,15 @@ int massive_output_bounds(const massive_ctx* c, int32_t n_seeds, int64_t* n_boun
   return MASSIVE_OK;
 }
 
-int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
+int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
   if (!c) return MASSIVE_EINVAL;
-  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier device failure");
+  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier failure");
   if (!io || n0 < 0 || (n0 > 0 && !seeds)) return c->fail(MASSIVE_EINVAL, "bad seeds / batch arguments");
   if (c->pending_round) return c->fail(MASSIVE_ESTATE, "massive_evict_step was not called after the last step");
   if (n0 > c->L) return c->fail(MASSIVE_EINVAL, "more seeds than local nodes");
+  const int slot = (int)(c->t & 1);
+  if (c->infl[slot].io) return c->fail(MASSIVE_ESTATE, "two batches in flight: wait for the older one first");
+  if (c->infl[slot ^ 1].io == io) return c->fail(MASSIVE_ESTATE, "this batch is still in flight");
   int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
   massive_output_bounds(c, n0, nb, eb);
   if (!io->nodes || !io->mask || !io->feat) return c->fail(MASSIVE_EINVAL, "nodes / mask / feat are NULL");
@@ -509,23 +543,28 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
   }
 
   hipStream_t s = c->s_main;
+  ms::StepSizes* sz = c->d_sz + slot;
+  int2* miss_list = c->d_miss_list[slot];
   const uint32_t key0 = (uint32_t)c->seed, key1 = (uint32_t)(c->seed >> 32);
-  CK(hipMemsetAsync(c->d_sz, 0, sizeof(ms::StepSizes), s));
+  // this parity's sizes and miss list were last used by the side stream two
+  // steps ago (complete: that batch was waited for)
+  CK(hipStreamWaitEvent(s, c->ev_batch_done[slot], 0));
+  CK(hipMemsetAsync(sz, 0, sizeof(ms::StepSizes), s));
   {
     massive_ctx::Range tr(c, s, 0);
     if (n0 > 0)
-      ms::k_seed_init<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, io->nodes, c->d_pos_of, c->d_sz);
+      ms::k_seed_init<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, io->nodes, c->d_pos_of, sz);
     for (int k = 1; k <= c->K; ++k) {
       const int64_t nprev = nb[k - 1];
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
-      ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, c->d_sz, k, c->fo[k - 1],
+      ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, sz, k, c->fo[k - 1],
                                                               io->indptr[k - 1], c->d_part, c->d_big, c->big_min);
-      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_sz, k, io->indptr[k - 1], c->d_part);
+      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(sz, k, io->indptr[k - 1], c->d_part);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;
       sa.nodes = io->nodes;
-      sa.sz = c->d_sz;
+      sa.sz = sz;
       sa.bptr = io->indptr[k - 1];
       sa.out = io->indices[k - 1];
       sa.hop = k;
@@ -533,7 +572,7 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
       sa.t = (uint32_t)c->t;
       sa.key0 = key0;
       sa.key1 = key1;
-      sa.err = &c->d_sz->status;
+      sa.err = &sz->status;
       sa.mu32 = c->mu32[k - 1];
       sa.big_min = c->big_min;
       sa.big_rows = c->d_big;
@@ -543,17 +582,29 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
       ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
                      s>>>(sa);
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, k, c->d_part);
-      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->d_sz, k, c->d_part, io->nodes,
+      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_part);
+      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_part, io->nodes,
                                                              c->d_pos_of);
-      ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], c->d_sz, k, c->d_pos_of);
+      ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], sz, k, c->d_pos_of);
+    }
+  }
+  // A refill that may still be in flight: hits on its slots read the host
+  // store instead (same bytes); once it has landed the buffer serves them.
+  int32_t pend = -1;
+  if (c->refill_inflight) {
+    if (hipEventQuery(c->ev_refill_done) == hipSuccess) {
+      c->refill_inflight = false;
+      CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
+    } else {
+      (void)hipGetLastError();
+      pend = c->round_id;
     }
   }
   {
     massive_ctx::Range tr(c, s, 1);
     ms::ClassifyArgs ca;
     ca.nodes = io->nodes;
-    ca.sz = c->d_sz;
+    ca.sz = sz;
     ca.K = c->K;
     ca.L = c->L;
     ca.tab = c->d_tab;
@@ -563,29 +614,59 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
     ca.pos_of = c->d_pos_of;
     ca.mask = io->mask;
     ca.hbm_list = c->d_hbm_list;
-    ca.miss_list = c->d_miss_list;
+    ca.miss_list = miss_list;
+    ca.slot_round = c->d_slot_round;
+    ca.pend_round = pend;
     ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, 4096), ms::kClsNT, 0, s>>>(ca);
   }
+  if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of, sz);
   // HBM rows first, at full bandwidth; the host-link rows follow on the side
-  // stream (concurrent host reads would throttle the HBM gather).
-  if (c->refill_pending) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
-  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &c->d_sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
-  CK(hipEventRecord(c->ev_classified, s));
-  CK(hipStreamWaitEvent(c->s_miss, c->ev_classified, 0));
+  // stream (concurrent host reads would throttle the HBM gather) and overlap
+  // whatever the main stream does next.
+  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
+  CK(hipEventRecord(c->ev_hbm_done[slot], s));
+  CK(hipStreamWaitEvent(c->s_miss, c->ev_hbm_done[slot], 0));
   if (c->H > 0)
-    launch_gather(c, 3, kMiss, c->s_miss, c->d_miss_list, &c->d_sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb,
-                  nb[c->K], c->host_blocks);
-  CK(hipEventRecord(c->ev_miss_done, c->s_miss));
-  CK(hipStreamWaitEvent(s, c->ev_miss_done, 0));
-  CK(hipMemcpyAsync(c->h_sz, c->d_sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, s));
+    launch_gather(c, 3, kMiss, c->s_miss, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
+                  c->host_blocks);
+  CK(hipMemcpyAsync(c->h_sz + slot, sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, c->s_miss));
+  CK(hipMemcpyAsync(c->h_bad + slot, &c->d_ctr->bad, sizeof(int32_t), hipMemcpyDeviceToHost, c->s_miss));
+  CK(hipEventRecord(c->ev_batch_done[slot], c->s_miss));
   CK(hipGetLastError());
-  CK(hipStreamSynchronize(s));
-  c->refill_pending = false;
-  const ms::StepSizes& z = *c->h_sz;
+  c->infl[slot].io = io;
+  c->infl[slot].step = c->t;
+  c->infl[slot].seeds = seeds;
+  c->infl[slot].n0 = n0;
+  c->t += 1;
+  c->pending_round = true;
+  return MASSIVE_OK;
+}
+
+int massive_batch_wait(massive_ctx* c, massive_batch* io) {
+  if (!c || !io) return MASSIVE_EINVAL;
+  int slot = -1;
+  for (int i = 0; i < 2; ++i)
+    if (c->infl[i].io == io) slot = i;
+  if (slot < 0) return c->fail(MASSIVE_EINVAL, "this batch is not in flight");
+  const massive_ctx::InFlight f = c->infl[slot];
+  c->infl[slot] = massive_ctx::InFlight();
+  CK(hipEventSynchronize(c->ev_batch_done[slot]));
+  const ms::StepSizes& z = c->h_sz[slot];
+  if (c->h_bad[slot]) {
+    c->broken = true;
+    return c->fail(MASSIVE_EHIP, "an eviction round produced inconsistent indices");
+  }
   if (z.status & 3) {
-    if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of);
-    CK(hipStreamSynchronize(s));
-    return c->fail(MASSIVE_EINVAL, (z.status & 1) ? "a seed is not a local node id" : "a seed is repeated");
+    // the step left no trace on the device; it can be taken back if nothing
+    // was issued after it
+    const char* why = (z.status & 1) ? "a seed is not a local node id" : "a seed is repeated";
+    if (f.step == c->t - 1 && c->pending_round && !c->infl[slot ^ 1].io) {
+      c->t -= 1;
+      c->pending_round = false;
+      return c->fail(MASSIVE_EINVAL, "%s", why);
+    }
+    c->broken = true;
+    return c->fail(MASSIVE_EINVAL, "%s (later work was already issued: context unusable)", why);
   }
   if (z.status) {
     c->broken = true;
@@ -596,101 +677,106 @@ int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_bat
   io->local = z.local;
   io->hits = z.hits;
   io->misses = z.misses;
-  c->t += 1;
-  c->pending_round = true;
-  if (c->timing) c->resolve_timing();
   return MASSIVE_OK;
 }
 
+int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
+  int rc = massive_sample_async(c, seeds, n0, io);
+  if (rc != MASSIVE_OK) return rc;
+  return massive_batch_wait(c, io);
+}
+
 int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t* replaced, int64_t* k_out) {
-  if (!c || !k_out) return MASSIVE_EINVAL;
-  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier device failure");
+  if (!c) return MASSIVE_EINVAL;
+  if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier failure");
   if (!c->pending_round) return c->fail(MASSIVE_ESTATE, "no sampled step owes an eviction round");
-  c->pending_round = false;
-  *k_out = 0;
+  if (k_out) *k_out = 0;
   const int64_t tl = c->t - 1;
-  if (!(tl > 0 && tl % c->delta == 0)) return MASSIVE_OK;
-  if (c->cap == 0) return MASSIVE_OK;
+  if (!(tl > 0 && tl % c->delta == 0) || c->cap == 0) {
+    c->pending_round = false;
+    return MASSIVE_OK;
+  }
   for (const void* p : {(const void*)evicted, (const void*)slots, (const void*)replaced})
     if (p && !device_visible(p)) return c->fail(MASSIVE_EINVAL, "an eviction output is not HIP-visible memory");
+  c->pending_round = false;
   hipStream_t s = c->s_main;
   const int64_t cap = c->cap, H = c->H;
-  int64_t kk = 0;
+  ms::RoundState* rs = c->d_rs;
+  // one refill in flight at a time: the previous one reads the fill list, the
+  // round state and the slot stamps that this round rewrites
+  if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
+  c->refill_inflight = false;
   {
     massive_ctx::Range tr(c, s, 4);
     ms::k_materialize<<<grid_for(cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, cap, (int32_t)(c->t - c->mat_t),
                                                           c->gamma);
     c->mat_t = c->t;
-    CK(hipMemsetAsync(c->d_rs, 0, sizeof(ms::RoundState), s));
+    CK(hipMemsetAsync(rs, 0, sizeof(ms::RoundState), s));
     const int64_t nbe = std::max<int64_t>(1, cdiv(cap, ms::kScanTile));
-    ms::k_evict_count<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part);
-    ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbe, &c->d_rs->nE, nullptr);
+    ms::k_evict_count<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part, &rs->nE);
     ms::k_evict_emit<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part, c->d_E);
-    ms::k_count_candidates<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, &c->d_rs->nC);
-    CK(hipMemcpyAsync(c->h_rs, c->d_rs, sizeof(ms::RoundState), hipMemcpyDeviceToHost, s));
-    CK(hipStreamSynchronize(s));
-    const int64_t nE = c->h_rs->nE, nC = c->h_rs->nC;
-    kk = std::min(nE, nC);
-    if (kk > 0) {
-      c->h_rs->k = kk;
-      c->h_rs->need = kk;
-      c->h_rs->prefix = 0;
-      c->h_rs->pmask = 0;
-      CK(hipMemcpyAsync(c->d_rs, c->h_rs, sizeof(ms::RoundState), hipMemcpyHostToDevice, s));
-      if (kk < nE) {
-        // fewer candidates than evictions: keep the kk slots of smallest (S_E, rank)
-        const int64_t* nEp = &c->d_rs->nE;
-        ms::k_esel_keys_lo<<<grid_for(nE, 256), 256, 0, s>>>(c->d_E, nEp, c->d_slot_id, c->d_rank_of, c->d_k0, c->d_v0);
-        sort_u32(c, s, nEp, 0, cap, nullptr);
-        ms::k_esel_keys_hi<<<grid_for(nE, 256), 256, 0, s>>>(c->d_v0, nEp, c->d_S_E, c->d_k0);
-        sort_u32(c, s, nEp, 0, cap, nullptr);
-        ms::k_esel_keys_slot<<<grid_for(kk, 256), 256, 0, s>>>(c->d_v0, &c->d_rs->k, c->d_k0);
-        sort_u32(c, s, &c->d_rs->k, 0, cap, c->d_E);
-      }
-      ms::k_fill<int32_t><<<grid_for(kk, 256), 256, 0, s>>>(c->d_R, kk, -1);
-      // radix select of the kk-th candidate key, 8 bits per pass
-      for (int shift = 24; shift >= 0; shift -= 8) {
-        ms::k_select_hist<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, c->d_rs, shift, c->d_ghist);
-        ms::k_select_pick<<<1, 256, 0, s>>>(c->d_rs, c->d_ghist, shift);
-      }
-      const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
-      ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, c->d_rs, c->d_part,
-                                                             c->d_part2);
-      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part, nbh, &c->d_rs->n_lt, nullptr);
-      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_part2, nbh, &c->d_rs->n_eq, nullptr);
-      ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, c->d_rs, c->d_part,
-                                                            c->d_part2, c->d_k0, c->d_v0, c->d_R);
-      // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
-      sort_u32(c, s, &c->d_rs->n_lt, 0, cap, c->d_R);
-      ms::k_swap<<<grid_for(kk, 256), 256, 0, s>>>(c->d_E, c->d_R, &c->d_rs->k, c->L, cap, c->H, c->d_slot_id,
-                                                   c->d_S_E, c->d_S_A, evicted, slots, replaced, c->d_fill,
-                                                   &c->d_rs->bad);
-      ms::k_fill<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty);
-      ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap);
+    ms::k_count_candidates<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, &rs->nC);
+    ms::k_round_setup<<<1, 1, 0, s>>>(rs, c->d_ctr);
+    // fewer candidates than evictions (only when f > 50%): keep the k' slots of
+    // smallest (S_E, rank); every kernel here sees zero elements otherwise
+    ms::k_esel_keys_lo<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, &rs->nE_sel, c->d_slot_id, c->d_rank_of, c->d_k0,
+                                                          c->d_v0);
+    sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
+    ms::k_esel_keys_hi<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->nE_sel, c->d_S_E, c->d_k0);
+    sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
+    ms::k_esel_keys_slot<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->k_sel, c->d_k0);
+    sort_u32(c, s, &rs->k_sel, 0, cap, c->d_E);
+    ms::k_fill_gated<int32_t><<<grid_for(cap, 256), 256, 0, s>>>(c->d_R, cap, -1, &rs->k);
+    // radix select of the k'-th candidate key, 8 bits per pass
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      ms::k_select_hist<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, rs, shift, c->d_ghist);
+      ms::k_select_pick<<<1, 256, 0, s>>>(rs, c->d_ghist, shift, &c->d_ctr->bad);
     }
+    const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
+    ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2);
+    ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2,
+                                                          c->d_k0, c->d_v0, c->d_R);
+    // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
+    sort_u32(c, s, &rs->n_lt, 0, cap, c->d_R);
+    c->round_id += 1;
+    ms::k_swap<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, c->d_R, &rs->k, c->L, cap, c->H, c->d_slot_id, c->d_S_E,
+                                                  c->d_S_A, evicted, slots, replaced, c->d_fill, &c->d_ctr->bad,
+                                                  c->d_slot_round, c->round_id);
+    ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
+    ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
   }
-  if (kk > 0) {
-    CK(hipMemcpyAsync(&c->h_rs->bad, &c->d_rs->bad, 4, hipMemcpyDeviceToHost, s));
+  CK(hipEventRecord(c->ev_swap_done, s));
+  CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
+  launch_gather(c, 5, kRefill, c->s_copy, c->d_fill, &rs->k, c->d_store, c->d_slab, c->rb, cap, c->host_blocks);
+  CK(hipEventRecord(c->ev_refill_done, c->s_copy));
+  c->refill_inflight = true;
+  CK(hipGetLastError());
+  if (k_out) {
+    CK(hipMemcpyAsync(&c->h_rs->k, &rs->k, 8, hipMemcpyDeviceToHost, s));
+    CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
     CK(hipStreamSynchronize(s));
-    if (c->h_rs->bad) {
+    if (c->h_ctr->bad) {
       c->broken = true;
       return c->fail(MASSIVE_EHIP, "eviction round produced inconsistent indices");
     }
-    CK(hipEventRecord(c->ev_swap_done, s));
-    CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
-    launch_gather(c, 5, kRefill, c->s_copy, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, c->rb, kk,
-                  c->host_blocks);
-    CK(hipEventRecord(c->ev_refill_done, c->s_copy));
-    c->refill_pending = true;
+    *k_out = c->h_rs->k;
   }
-  CK(hipGetLastError());
-  *k_out = kk;
+  return MASSIVE_OK;
+}
+
+int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted) {
+  if (!c) return MASSIVE_EINVAL;
+  CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, c->s_main));
+  CK(hipStreamSynchronize(c->s_main));
+  if (rounds) *rounds = c->h_ctr->rounds;
+  if (evicted) *evicted = c->h_ctr->evicted;
   return MASSIVE_OK;
 }
 
 int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, int64_t* t) {
   if (!c) return MASSIVE_EINVAL;
   hipStream_t s = c->s_main;
+  CK(hipStreamSynchronize(c->s_miss));
   if (c->cap > 0 && c->t > c->mat_t) {
     ms::k_materialize<<<grid_for(c->cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, c->cap,
                                                              (int32_t)(c->t - c->mat_t), c->gamma);
@@ -706,7 +792,7 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
 
 int massive_get_buffer_rows(massive_ctx* c, void* out) {
   if (!c || (!out && c->cap)) return MASSIVE_EINVAL;
-  if (c->refill_pending) CK(hipStreamWaitEvent(c->s_main, c->ev_refill_done, 0));
+  if (c->refill_inflight) CK(hipStreamWaitEvent(c->s_main, c->ev_refill_done, 0));
   if (c->cap)
     CK(hipMemcpyAsync(out, c->d_slab + (int64_t)c->L * c->rb, c->cap * c->rb, hipMemcpyDeviceToHost, c->s_main));
   CK(hipStreamSynchronize(c->s_main));

@@ -18,9 +18,10 @@ MAX_HOPS = 8
 OK, EINVAL, ECAPACITY, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
 _NAMES = {EINVAL: "EINVAL", ECAPACITY: "ECAPACITY", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE"}
 
-EXPORTS = ("massive_init", "massive_output_bounds", "massive_sample", "massive_evict_step",
-           "massive_get_state", "massive_get_buffer_rows", "massive_info", "massive_set_timing",
-           "massive_get_timing", "massive_destroy", "massive_last_error")
+EXPORTS = ("massive_init", "massive_output_bounds", "massive_sample", "massive_sample_async",
+           "massive_batch_wait", "massive_evict_step", "massive_get_counters", "massive_get_state",
+           "massive_get_buffer_rows", "massive_info", "massive_set_timing", "massive_get_timing",
+           "massive_destroy", "massive_last_error")
 
 
 class MassiveError(RuntimeError):
@@ -66,7 +67,10 @@ def load():
     lib.massive_init.argtypes = [P(InitArgs), P(vp)]
     lib.massive_output_bounds.argtypes = [vp, i32, vp, vp]
     lib.massive_sample.argtypes = [vp, vp, i32, P(Batch)]
-    lib.massive_evict_step.argtypes = [vp, vp, vp, vp, P(i64)]
+    lib.massive_sample_async.argtypes = [vp, vp, i32, P(Batch)]
+    lib.massive_batch_wait.argtypes = [vp, P(Batch)]
+    lib.massive_evict_step.argtypes = [vp, vp, vp, vp, vp]
+    lib.massive_get_counters.argtypes = [vp, P(i64), P(i64)]
     lib.massive_get_state.argtypes = [vp, vp, vp, vp, P(i64)]
     lib.massive_get_buffer_rows.argtypes = [vp, vp]
     lib.massive_info.argtypes = [vp, P(i64), P(ctypes.c_float)]
@@ -212,13 +216,36 @@ class Massive:
         return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
                           local=int(c.local), hits=int(c.hits), misses=int(c.misses))
 
-    def evict_step(self, out=None) -> int:
+    def sample_async(self, seeds, bb: BatchBuffers) -> None:
+        """Enqueues one step; bb must not be touched until wait(bb)."""
+        n0 = int(seeds.numel())
+        bb._seeds = seeds  # keep the seed tensor alive while the step is in flight
+        self._check(self._lib.massive_sample_async(self._h, seeds.data_ptr() if n0 else None, n0,
+                                                   ctypes.byref(bb.c)))
+
+    def wait(self, bb: BatchBuffers) -> StepResult:
+        self._check(self._lib.massive_batch_wait(self._h, ctypes.byref(bb.c)))
+        bb._seeds = None
+        c = bb.c
+        return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
+                          local=int(c.local), hits=int(c.hits), misses=int(c.misses))
+
+    def evict_step(self, out=None, wait: bool = True) -> int:
         """Runs the round owed by the last step; out = (evicted, slots, replaced)
-        int32 device tensors with room for cap entries, or None."""
-        k = ctypes.c_int64()
+        int32 device tensors with room for cap entries, or None. wait=False
+        only enqueues it (returns -1)."""
         ev, sl, rp = (None, None, None) if out is None else tuple(_ptr(x) for x in out)
+        if not wait:
+            self._check(self._lib.massive_evict_step(self._h, ev, sl, rp, None))
+            return -1
+        k = ctypes.c_int64()
         self._check(self._lib.massive_evict_step(self._h, ev, sl, rp, ctypes.byref(k)))
         return int(k.value)
+
+    def counters(self):
+        r, e = ctypes.c_int64(), ctypes.c_int64()
+        self._check(self._lib.massive_get_counters(self._h, ctypes.byref(r), ctypes.byref(e)))
+        return int(r.value), int(e.value)
 
     def state(self):
         sid = np.zeros(max(self.cap, 1), np.int32)

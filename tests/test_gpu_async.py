@@ -1,0 +1,88 @@
+"""GPU parity of the look-ahead pipeline: massive_sample_async with two batches
+in flight and eviction rounds enqueued without waiting, against the oracle
+run step by step. With a short eviction interval on the products-sized graph
+the refills (hundreds of thousands of rows over the host link) are still in
+flight when the next steps classify, so hits on refilled slots are served
+from the host store; the outputs must not change."""
+import numpy as np
+import pytest
+
+from gpu_util import compare_state, compare_step, log, make_gpu, require_gpu, to_dev
+from helpers import workload_problem
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def run_lookahead(name, prob, seeds_of, steps):
+    import torch
+    orc = prob.oracle()
+    gm = make_gpu(prob)
+    K = len(prob.fanout)
+    batch_max = max(len(seeds_of(t)) for t in range(steps))
+    bbs = [gm.alloc_batch(batch_max), gm.alloc_batch(batch_max)]
+    cap = gm.cap
+    outs = [tuple(torch.full((max(cap, 1),), -7, dtype=torch.int32, device="cuda") for _ in range(3))
+            for _ in range(steps)]
+    seeds_dev = [to_dev(seeds_of(t)) for t in range(steps)]
+    rounds_o, evicted_o = [], 0
+
+    def check(t):
+        res = gm.wait(bbs[t % 2])
+        st = orc.sample(seeds_of(t))
+        compare_step("%s t=%d" % (name, t), st, res, bbs[t % 2], K)
+        ro = orc.evict_step()
+        rounds_o.append(ro)
+        return ro.k
+
+    for t in range(steps):
+        log("%s t=%d enqueue" % (name, t))
+        gm.sample_async(seeds_dev[t], bbs[t % 2])
+        gm.evict_step(outs[t], wait=False)
+        if t >= 1:
+            k = check(t - 1)
+            evicted_o += k
+    evicted_o += check(steps - 1)
+    torch.cuda.synchronize()
+    n_rounds = 0
+    for t, ro in enumerate(rounds_o):
+        if ro.k:
+            n_rounds += 1
+            ev, sl, rp = (x[:ro.k].cpu().numpy() for x in outs[t])
+            assert np.array_equal(sl, ro.slots) and np.array_equal(ev, ro.evicted) and np.array_equal(rp, ro.replaced), t
+    compare_state(name + " end", orc, gm)
+    assert np.array_equal(gm.buffer_rows(), orc.buffer_rows())
+    assert gm.counters() == (n_rounds, evicted_o)
+    log("%s: %d steps, %d rounds, %d evicted" % (name, steps, n_rounds, evicted_o))
+    return n_rounds
+
+
+def test_lookahead_cl10k():
+    prob, sched, w = workload_problem("cl10k", delta=3, gamma=0.8)
+    assert run_lookahead("async cl10k", prob, sched.seeds, 24) >= 3
+
+
+def test_lookahead_cl2m45_inflight_refills():
+    prob, sched, w = workload_problem("cl2m45", delta=2)
+    assert run_lookahead("async cl2m45", prob, sched.seeds, 6) == 2
+
+
+def test_lookahead_rejects_a_third_batch():
+    from paper_2410_22697_amd import MassiveError
+    prob, sched, w = workload_problem("cl10k")
+    gm = make_gpu(prob)
+    bbs = [gm.alloc_batch(w.batch) for _ in range(3)]
+    s = [to_dev(sched.seeds(t)) for t in range(3)]
+    gm.sample_async(s[0], bbs[0])
+    gm.evict_step(wait=False)
+    gm.sample_async(s[1], bbs[1])
+    gm.evict_step(wait=False)
+    with pytest.raises(MassiveError) as ei:
+        gm.sample_async(s[2], bbs[2])
+    assert ei.value.code == -5
+    gm.wait(bbs[0])
+    gm.wait(bbs[1])
