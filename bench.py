@@ -58,6 +58,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--threads", type=int, default=None)
     ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
+    ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
+    ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
+    ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -71,6 +74,10 @@ def main():
     from paper_2410_22697_amd import Massive
 
     w = synth.get(args.workload)
+    over = {k: v for k, v in (("delta", args.delta), ("gamma", args.gamma), ("buffer_pct", args.buffer_pct))
+            if v is not None}
+    if over:
+        w = w.with_(**over)
     g, local, store, sched = build_inputs(w, args.threads)
     torch.cuda.set_device(0)
     t0 = time.time()
@@ -106,7 +113,7 @@ def main():
                 gm.evict_step(wait=False)
             if prev is not None:
                 r = gm.wait(bbs[prev % 2])
-                stats.append((r.local, r.hits, r.misses, r.n[-1]))
+                stats.append((r.local, r.hits, r.misses, r.n[-1], r.host_rows))
                 if prev < 2 and len(first_steps) == prev:
                     bb = bbs[prev % 2]
                     nK = r.n[-1]
@@ -145,9 +152,14 @@ def main():
     g_avg_s = g_ms / 1e3 / max(g_calls, 1)
     g_gbps = g_bytes_per_launch / g_avg_s / 1e9
     m_ms, m_calls = tim["gather_miss"]
-    m_bytes = float(np.mean(mis * rb))
+    host_rows = np.array([s[4] for s in stats], np.float64)
+    m_bytes = float(np.mean(host_rows * rb))
     m_gbps = m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9
     hit_rate = float(hit.sum() / max(hit.sum() + mis.sum(), 1))
+    rf_ms, rf_calls = tim["refill"]
+    log("host link per step: %.1f MB miss gather (%.1f MB of them hits on refilling slots), "
+        "%.1f MB refill (amortised)" % (m_bytes / 1e6, float(np.mean((host_rows - mis) * rb)) / 1e6,
+                                        evicted * rb / max(K, 1) / 1e6))
     for name, (ms, calls) in tim.items():
         log("  %-13s %9.3f ms total, %5d launches, %.1f us avg" % (name, ms, calls, 1e3 * ms / max(calls, 1)))
     log("gather_hbm %.0f B/launch, %.1f us, %.1f GB/s (%.1f%% of HBM); miss fetch %.1f GB/s; hit rate %.3f" %

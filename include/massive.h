@@ -113,6 +113,9 @@ typedef struct {
   int64_t n[MASSIVE_MAX_HOPS + 1];         /* frontier sizes n_0..n_K              */
   int64_t e[MASSIVE_MAX_HOPS];             /* sampled edges per hop                */
   int64_t local, hits, misses;             /* input rows by class (unique nodes)   */
+  int64_t host_rows;                       /* rows read over the host link: the
+                                              misses, plus hits on slots whose
+                                              refill had not landed yet        */
 } massive_batch;
 
 /* One minibatch at the context's current step t: samples K hops from the

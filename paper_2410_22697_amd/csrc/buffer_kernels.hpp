@@ -70,6 +70,7 @@ struct ClassifyArgs {
   int2* hbm_list;
   int2* miss_list;
   const int32_t* slot_round;  // round that last refilled each slot
+  const int32_t* landed;      // round whose refill row has landed in each slot
   int32_t pend_round;         // refill of this round may still be in flight (-1: none)
 };
 
@@ -111,7 +112,8 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
             a.hitcnt[slot] += 1;
             // a hit on a slot whose refill may not have landed reads the same
             // row from the host store
-            if (a.pend_round >= 0 && a.slot_round[slot] == a.pend_round) {
+            if (a.pend_round >= 0 && a.slot_round[slot] == a.pend_round &&
+                __hip_atomic_load(&a.landed[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.pend_round) {
               cls[it] = 3;
               src[it] = h;
             }
@@ -229,12 +231,57 @@ __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ li
                                                      int64_t rb, uint32_t cpr, uint64_t magic) {
   gather_body<V>(list, count, src, dst, rb, cpr, magic);
 }
-// eviction refill: pinned host store -> buffer slots
+// Eviction refill: pinned host store -> buffer slots, row by row (G lanes
+// per row), in list order (replacements of highest S_A first), kRefillRows
+// rows in flight per lane group. Each batch of rows is then published:
+// release fence, then landed[slot] = round, which classify reads to serve hits
+// on those slots from HBM. (The fence waits for every store of the batch, so
+// batches are large.)
+constexpr int kRefillRows = 16;
+
 template <typename V>
 __global__ __launch_bounds__(256) void k_refill(const int2* __restrict__ list, const int64_t* __restrict__ count,
                                                 const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                                int64_t rb, uint32_t cpr, uint64_t magic) {
-  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+                                                int64_t rb, uint32_t cpr, uint32_t G, int32_t L,
+                                                int32_t* __restrict__ landed, int32_t round_id, int32_t chunk,
+                                                int32_t nchunks) {
+  // this launch refills fill-list rows [lo, hi): chunk `chunk` of `nchunks`
+  const int64_t k = *count;
+  const int64_t lo = k * chunk / nchunks, hi = k * (chunk + 1) / nchunks;
+  const int64_t n = hi - lo;
+  list += lo;
+  const int lane = lane_id();
+  const int rpw = MS_WAVE / (int)G;  // row slots per wave
+  const int sub = lane / (int)G, cl = lane % (int)G;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / MS_WAVE;
+  const int64_t nwaves = (int64_t)gridDim.x * blockDim.x / MS_WAVE;
+  const int64_t per = (int64_t)kRefillRows * rpw;
+  for (int64_t base = wave * per; base < n; base += nwaves * per) {
+    int2 e[kRefillRows];
+    bool ok[kRefillRows];
+#pragma unroll
+    for (int u = 0; u < kRefillRows; ++u) {
+      const int64_t r = base + (int64_t)u * rpw + sub;
+      ok[u] = sub < rpw && r < n;
+      e[u] = ok[u] ? list[r] : make_int2(0, 0);
+      ok[u] = ok[u] && e[u].x >= L && e[u].y >= 0;  // entries flagged inconsistent by k_swap are skipped
+    }
+    for (uint32_t ch = cl; ch < cpr; ch += G) {
+      V v[kRefillRows];
+#pragma unroll
+      for (int u = 0; u < kRefillRows; ++u)
+        if (ok[u]) v[u] = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e[u].y * rb + (uint64_t)ch * sizeof(V));
+#pragma unroll
+      for (int u = 0; u < kRefillRows; ++u)
+        if (ok[u]) *reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e[u].x * rb + (uint64_t)ch * sizeof(V)) = v[u];
+    }
+    __threadfence();
+    if (cl == 0) {
+#pragma unroll
+      for (int u = 0; u < kRefillRows; ++u)
+        if (ok[u]) __hip_atomic_store(&landed[e[u].x - L], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 }
 
 // ------------------------------------------------------------ lazy decay

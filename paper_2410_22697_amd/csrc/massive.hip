@@ -56,7 +56,8 @@ struct massive_ctx {
   int64_t W = 0;        // bitmap words
   int64_t pmax = 0;     // partials capacity
   int64_t sort_cap = 0; // radix sort capacity
-  int64_t host_blocks = 16;  // grid of the host-link gathers
+  int64_t host_blocks = 16;   // grid of the miss gather (host link)
+  int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
   int32_t* d_big = nullptr;             // big-row list of the current hop
   int64_t big_min = ms::kBigRow;        // rows longer than this use the 16-wave kernel
@@ -65,8 +66,13 @@ struct massive_ctx {
   // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
   hipEvent_t ev_hbm_done[2] = {}, ev_batch_done[2] = {};
   hipEvent_t ev_swap_done = nullptr, ev_refill_done = nullptr;
-  bool refill_inflight = false;  // the last round's refill may not have landed
-  int32_t round_id = 0;          // rounds that swapped at least one slot, as stamped in slot_round
+  // The refill of the last round is copied in chunks, one after each of the
+  // next steps' HBM gathers (host-link reads never overlap an HBM gather).
+  int32_t round_id = 0;          // rounds so far, as stamped in slot_round / landed
+  int32_t refill_chunks = 1;     // chunks per round: min(delta, 32), one per step of the interval
+  int32_t chunks_left = 0;       // chunks of round_id's refill not yet launched
+  bool refill_inflight = false;  // a launched chunk may not have landed
+  bool round_pending_rows = false;  // round_id's refill not fully landed (hits may need the host)
   // device memory
   int64_t* d_indptr = nullptr;
   int32_t* d_indices = nullptr;
@@ -88,7 +94,8 @@ struct massive_ctx {
   ms::RoundState* h_rs = nullptr;     // pinned mailbox
   ms::Counters* d_ctr = nullptr;
   ms::Counters* h_ctr = nullptr;      // pinned
-  int32_t* d_slot_round = nullptr;    // [cap]
+  int32_t* d_slot_round = nullptr;    // [cap] round whose swap last filled the slot
+  int32_t* d_landed = nullptr;        // [cap] round whose refill row has landed
   int32_t* d_part = nullptr;
   int32_t* d_part2 = nullptr;
   int2* d_hbm_list = nullptr;
@@ -231,7 +238,7 @@ bool device_visible(const void* p) {
 }
 
 // the flattened gather, specialised on the widest vector the row allows
-enum GatherKind { kHbm, kMiss, kRefill };
+enum GatherKind { kHbm, kMiss };
 
 // The flattened row gather, specialised on the widest vector the row and
 // both base pointers allow. max_blocks bounds the grid: host-link gathers
@@ -265,10 +272,8 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
   do {                                     \
     if (kind == kHbm)                      \
       MS_LAUNCH(k_gather_hbm, V);          \
-    else if (kind == kMiss)                \
-      MS_LAUNCH(k_gather_miss, V);         \
     else                                   \
-      MS_LAUNCH(k_refill, V);              \
+      MS_LAUNCH(k_gather_miss, V);         \
   } while (0)
   if (vec == 16)
     MS_KIND(ms::v4u);
@@ -281,13 +286,69 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
   if (timed) c->pending.push_back({ea, eb, group});
 }
 
+// The refill: rows of the fill list copied from the host store into buffer
+// slots, each slot published in landed[] once its row is written.
+void launch_refill(massive_ctx* c, hipStream_t s, const int64_t* count, int64_t max_rows, int32_t round_id,
+                   int32_t chunk, int32_t nchunks) {
+  hipEvent_t ea = nullptr, eb = nullptr;
+  const bool timed = c->kernel_pair(&ea, &eb);
+  const uint8_t* src = c->d_store;
+  uint8_t* dst = c->d_slab;
+  const int64_t rb = c->rb;
+  int vec = 4;
+  if (rb % 16 == 0 && ((uintptr_t)src % 16) == 0 && ((uintptr_t)dst % 16) == 0)
+    vec = 16;
+  else if (rb % 8 == 0 && ((uintptr_t)src % 8) == 0 && ((uintptr_t)dst % 8) == 0)
+    vec = 8;
+  const uint32_t cpr = (uint32_t)(rb / vec);
+  uint32_t G = 1;
+  while (G < cpr && G < MS_WAVE) G <<= 1;
+  const int64_t rows_per_block = (256 / MS_WAVE) * ms::kRefillRows * (MS_WAVE / G);
+  const unsigned grid = grid_for(std::max<int64_t>(max_rows / nchunks + 1, 1), (int)rows_per_block, c->refill_blocks);
+#define MS_RF(V)                                                                                              \
+  do {                                                                                                        \
+    if (timed)                                                                                                \
+      hipExtLaunchKernelGGL(ms::k_refill<V>, dim3(grid), dim3(256), 0, s, ea, eb, 0, (const int2*)c->d_fill, count, \
+                            src, dst, rb, cpr, G, c->L, c->d_landed, round_id, chunk, nchunks);               \
+    else                                                                                                      \
+      ms::k_refill<V><<<grid, 256, 0, s>>>(c->d_fill, count, src, dst, rb, cpr, G, c->L, c->d_landed, round_id, \
+                                           chunk, nchunks);                                                  \
+  } while (0)
+  if (vec == 16)
+    MS_RF(ms::v4u);
+  else if (vec == 8)
+    MS_RF(ms::v2u);
+  else
+    MS_RF(unsigned int);
+#undef MS_RF
+  if (timed) c->pending.push_back({ea, eb, 5});
+}
+
+// Launches the next `count` pending refill chunks on the copy stream, after
+// event `after` (the HBM gather they must not overlap).
+int launch_refill_chunks(massive_ctx* c, int count, hipEvent_t after) {
+  while (count-- > 0 && c->chunks_left > 0) {
+    if (after) {
+      hipError_t e = hipStreamWaitEvent(c->s_copy, after, 0);
+      if (e != hipSuccess) return c->fail(MASSIVE_EHIP, "hipStreamWaitEvent: %s", hipGetErrorString(e));
+    }
+    const int32_t chunk = c->refill_chunks - c->chunks_left;
+    launch_refill(c, c->s_copy, &c->d_rs->k, c->cap, c->round_id, chunk, c->refill_chunks);
+    c->chunks_left -= 1;
+    hipError_t e = hipEventRecord(c->ev_refill_done, c->s_copy);
+    if (e != hipSuccess) return c->fail(MASSIVE_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+    c->refill_inflight = true;
+  }
+  return MASSIVE_OK;
+}
+
 void free_ctx(massive_ctx* c) {
   if (!c) return;
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
                  c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_E, c->d_R,
-                 c->d_fill, c->d_ctr, c->d_slot_round,
+                 c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
     if (p) (void)hipFree(p);
@@ -340,6 +401,9 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   }
 
   if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
+  if (const char* e = getenv("MASSIVE_REFILL_BLOCKS")) c->refill_blocks = std::max(1, atoi(e));
+  c->refill_chunks = std::min<int32_t>(a->delta, 32);
+  if (const char* e = getenv("MASSIVE_REFILL_CHUNKS")) c->refill_chunks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
@@ -377,6 +441,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_rs, sizeof(ms::RoundState));
   CKA(c->d_ctr, sizeof(ms::Counters));
   CKA(c->d_slot_round, cap * 4);
+  CKA(c->d_landed, cap * 4);
   CKA(c->d_part, c->pmax * 4);
   CKA(c->d_part2, c->pmax * 4);
   CKA(c->d_hbm_list, R * 8);
@@ -416,6 +481,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CK(hipMemsetAsync(c->d_ghist, 0, 256 * 4, s));
   CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
   CK(hipMemsetAsync(c->d_slot_round, 0xFF, cap * 4, s));
+  CK(hipMemsetAsync(c->d_landed, 0xFF, cap * 4, s));
 
   if (H > 0) {
     // halo rank: (degree desc, global id asc) by two stable radix sorts
@@ -443,7 +509,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
     // the cap best-ranked rows arrive over the host link
     c->h_rs->k = cap;
     CK(hipMemcpyAsync(&c->d_rs->k, &c->h_rs->k, 8, hipMemcpyHostToDevice, s));
-    launch_gather(c, 5, kRefill, s, c->d_fill, &c->d_rs->k, c->d_store, c->d_slab, rb, cap, c->host_blocks);
+    launch_refill(c, s, &c->d_rs->k, cap, 0, 0, 1);
   }
   // the step-parity events start out complete
   for (int i = 0; i < 2; ++i) {
@@ -591,10 +657,11 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   // A refill that may still be in flight: hits on its slots read the host
   // store instead (same bytes); once it has landed the buffer serves them.
   int32_t pend = -1;
-  if (c->refill_inflight) {
-    if (hipEventQuery(c->ev_refill_done) == hipSuccess) {
+  if (c->round_pending_rows) {
+    if (c->chunks_left == 0 && (!c->refill_inflight || hipEventQuery(c->ev_refill_done) == hipSuccess)) {
+      c->round_pending_rows = false;
+      if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
       c->refill_inflight = false;
-      CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
     } else {
       (void)hipGetLastError();
       pend = c->round_id;
@@ -616,6 +683,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ca.hbm_list = c->d_hbm_list;
     ca.miss_list = miss_list;
     ca.slot_round = c->d_slot_round;
+    ca.landed = c->d_landed;
     ca.pend_round = pend;
     ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, 4096), ms::kClsNT, 0, s>>>(ca);
   }
@@ -623,8 +691,16 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   // HBM rows first, at full bandwidth; the host-link rows follow on the side
   // stream (concurrent host reads would throttle the HBM gather) and overlap
   // whatever the main stream does next.
+  // no host-link reads while the HBM gather runs: the previous step's miss
+  // gather and the last refill chunk finish first
+  CK(hipStreamWaitEvent(s, c->ev_batch_done[slot ^ 1], 0));
+  if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
   launch_gather(c, 2, kHbm, s, c->d_hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
   CK(hipEventRecord(c->ev_hbm_done[slot], s));
+  {
+    int rc = launch_refill_chunks(c, 1, c->ev_hbm_done[slot]);
+    if (rc != MASSIVE_OK) return rc;
+  }
   CK(hipStreamWaitEvent(c->s_miss, c->ev_hbm_done[slot], 0));
   if (c->H > 0)
     launch_gather(c, 3, kMiss, c->s_miss, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
@@ -677,6 +753,7 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   io->local = z.local;
   io->hits = z.hits;
   io->misses = z.misses;
+  io->host_rows = z.n_miss;
   return MASSIVE_OK;
 }
 
@@ -702,10 +779,15 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   hipStream_t s = c->s_main;
   const int64_t cap = c->cap, H = c->H;
   ms::RoundState* rs = c->d_rs;
-  // one refill in flight at a time: the previous one reads the fill list, the
-  // round state and the slot stamps that this round rewrites
+  // the previous round's refill reads the fill list, the round state and the
+  // slot stamps that this round rewrites: finish it first
+  {
+    int rc = launch_refill_chunks(c, c->chunks_left, nullptr);
+    if (rc != MASSIVE_OK) return rc;
+  }
   if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
   c->refill_inflight = false;
+  c->round_pending_rows = false;
   {
     massive_ctx::Range tr(c, s, 4);
     ms::k_materialize<<<grid_for(cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, cap, (int32_t)(c->t - c->mat_t),
@@ -745,11 +827,11 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
   }
+  // the refill is copied in chunks after the next steps' HBM gathers
   CK(hipEventRecord(c->ev_swap_done, s));
   CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
-  launch_gather(c, 5, kRefill, c->s_copy, c->d_fill, &rs->k, c->d_store, c->d_slab, c->rb, cap, c->host_blocks);
-  CK(hipEventRecord(c->ev_refill_done, c->s_copy));
-  c->refill_inflight = true;
+  c->chunks_left = c->refill_chunks;
+  c->round_pending_rows = true;
   CK(hipGetLastError());
   if (k_out) {
     CK(hipMemcpyAsync(&c->h_rs->k, &rs->k, 8, hipMemcpyDeviceToHost, s));
@@ -792,6 +874,10 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
 
 int massive_get_buffer_rows(massive_ctx* c, void* out) {
   if (!c || (!out && c->cap)) return MASSIVE_EINVAL;
+  {
+    int rc = launch_refill_chunks(c, c->chunks_left, nullptr);
+    if (rc != MASSIVE_OK) return rc;
+  }
   if (c->refill_inflight) CK(hipStreamWaitEvent(c->s_main, c->ev_refill_done, 0));
   if (c->cap)
     CK(hipMemcpyAsync(out, c->d_slab + (int64_t)c->L * c->rb, c->cap * c->rb, hipMemcpyDeviceToHost, c->s_main));

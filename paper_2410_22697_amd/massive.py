@@ -47,7 +47,8 @@ class Batch(ctypes.Structure):
                 ("indptr", ctypes.c_void_p * MAX_HOPS), ("indices", ctypes.c_void_p * MAX_HOPS),
                 ("indptr_cap", ctypes.c_int64 * MAX_HOPS), ("indices_cap", ctypes.c_int64 * MAX_HOPS),
                 ("n", ctypes.c_int64 * (MAX_HOPS + 1)), ("e", ctypes.c_int64 * MAX_HOPS),
-                ("local", ctypes.c_int64), ("hits", ctypes.c_int64), ("misses", ctypes.c_int64)]
+                ("local", ctypes.c_int64), ("hits", ctypes.c_int64), ("misses", ctypes.c_int64),
+                ("host_rows", ctypes.c_int64)]
 
 
 _lib = None
@@ -117,6 +118,7 @@ class StepResult:
     local: int
     hits: int
     misses: int
+    host_rows: int = 0
 
 
 class Massive:
@@ -214,7 +216,7 @@ class Massive:
                                              ctypes.byref(bb.c)))
         c = bb.c
         return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
-                          local=int(c.local), hits=int(c.hits), misses=int(c.misses))
+                          local=int(c.local), hits=int(c.hits), misses=int(c.misses), host_rows=int(c.host_rows))
 
     def sample_async(self, seeds, bb: BatchBuffers) -> None:
         """Enqueues one step; bb must not be touched until wait(bb)."""
@@ -228,7 +230,7 @@ class Massive:
         bb._seeds = None
         c = bb.c
         return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
-                          local=int(c.local), hits=int(c.hits), misses=int(c.misses))
+                          local=int(c.local), hits=int(c.hits), misses=int(c.misses), host_rows=int(c.host_rows))
 
     def evict_step(self, out=None, wait: bool = True) -> int:
         """Runs the round owed by the last step; out = (evicted, slots, replaced)
