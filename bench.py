@@ -27,6 +27,23 @@ HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
 PCIE_PEAK_GBPS = 64.0        # PCIe 5.0 x16, one direction
 
 
+def gather_traffic(rb_per_launch):
+    """HBM bytes per gather_hbm launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), as a ratio to
+    the algorithmic bytes applied to this run's launches; None if the gather
+    kernel's source has changed since the counters were taken."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "gather_hbm_cl111m_p64_hbm_counters.txt")
+    src = open(os.path.join(ROOT, "paper_2410_22697_amd", "csrc", "buffer_kernels.hpp")).read()
+    a, b = src.find("__device__ __forceinline__ void gather_body"), src.find("// misses: pinned host store")
+    if not os.path.exists(prof) or a < 0 or b < 0:
+        return None
+    kv = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if l.startswith(("traffic_", "gather_source")))
+    if kv.get("gather_source_sha256") != hashlib.sha256(src[a:b].encode()).hexdigest():
+        return None
+    return round(float(kv["traffic_over_algorithmic"]) * rb_per_launch)
+
+
 def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
@@ -191,7 +208,8 @@ def main():
         "gather_frac_hbm": round(g_gbps / HBM_PEAK_GBPS, 4),
         "hit_rate": round(hit_rate, 4),
         "roofline": {"bound": "hbm", "kernel": "gather_hbm", "achieved": round(g_gbps, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(g_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(g_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": gather_traffic(g_bytes_per_launch) if w.name == "cl111m_p64" else None,
                      "bytes_per_launch": round(g_bytes_per_launch), "avg_us": round(g_avg_s * 1e6, 2)},
         "host_link": {"kernel": "gather_miss", "achieved": round(m_gbps, 2), "peak": PCIE_PEAK_GBPS,
                       "unit": "GB/s", "bytes_per_launch": round(m_bytes),
