@@ -1,6 +1,7 @@
 """Full-size checks on the papers-sized share (partition 0 of 64 of a
-111M-node Chung-Lu graph): the workload and launch configuration the bench
-times. The whole-run oracle is too slow here (tens of seconds per step), so
+111M-node Chung-Lu graph: the workload and launch configuration the bench
+times) and on the products-sized configurations (fp32 and the bf16 stress
+setting). The whole-run oracle is too slow here (tens of seconds per step), so
 every checked step is verified on outputs the oracle computes one by one and
 on properties that hold at any size:
   * sampled rows: each checked row equals the oracle's choice for that row
@@ -10,7 +11,7 @@ on properties that hold at any size:
   * masks: every row's class against the buffer as it stood before the step;
   * features: gathered bytes equal the source rows (local slab / host store);
   * scores: S_A += 1 on misses, S_E *= gamma (fp32) on unsampled slots;
-  * the eviction round at t = 32: E, the replacements (a numpy lexsort of the
+  * an eviction round: E, the replacements (a numpy lexsort of the
     candidates), the score swap and the refilled rows.
 The steps between checked ones run with look-ahead, as in the bench.
 """
@@ -26,11 +27,12 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1200)]
 _W = {}
 
 
-def _inputs():
-    if "g" not in _W:
+def _inputs(name):
+    if _W.get("name") != name:
         import torch
         import synth
-        w = synth.get("cl111m_p64")
+        _W.clear()
+        w = synth.get(name)
         t0 = time.time()
         log("generating %s" % w.name)
         g = synth.partition_graph(w)
@@ -41,7 +43,8 @@ def _inputs():
         store = torch.empty((g.H, rb), dtype=torch.uint8, pin_memory=True)
         synth.fill_features(g.halo_gid, w.d, w.dtype, w.seed, store.data_ptr())
         log("features done (%.0fs)" % (time.time() - t0))
-        _W.update(w=w, g=g, local=local, store=store, sched=synth.Schedule(g.L, w.train_pct, w.batch, w.seed))
+        _W.update(name=name, w=w, g=g, local=local, store=store,
+                  sched=synth.Schedule(g.L, w.train_pct, w.batch, w.seed))
     return _W
 
 
@@ -98,11 +101,18 @@ def _check_step(tag, gm, bb, res, seeds, t, w, g, local, store_np, pre, rng):
     assert np.array_equal(se2.view(np.uint32), se_want.view(np.uint32)), tag + " S_E"
 
 
-def test_papers_share_full_size():
+# (workload, steps checked one by one, the round step whose selection is checked)
+CASES = [("cl111m_p64", (0, 1, 2, 31, 32, 33), 32),    # papers-sized share, delta 32
+         ("cl2m45", (0, 1, 31, 32, 33), 32),            # products-sized, delta 32, 7 minibatches per epoch
+         ("cl2m45_bf16", (0, 1, 3, 4, 5, 8, 9), 4)]     # bf16 rows, f 50%, gamma 0.8, delta 4, batch 4096
+
+
+@pytest.mark.parametrize("name,checked,round_t", CASES)
+def test_full_size(name, checked, round_t):
     require_gpu()
     import torch
     from paper_2410_22697_amd import Massive
-    W = _inputs()
+    W = _inputs(name)
     w, g, local, store, sched = W["w"], W["g"], W["local"], W["store"], W["sched"]
     store_np = store.numpy()
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
@@ -116,18 +126,19 @@ def test_papers_share_full_size():
     assert np.array_equal(gm.buffer_rows()[:: max(1, gm.cap // 20000)],
                           store_np[sid0[:: max(1, gm.cap // 20000)]])
     bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
-    checked = {0, 1, 2, 31, 32, 33}
+    checked = set(checked)
+    last = max(checked) + 1
     cap = gm.cap
     ev, sl, rp = (torch.empty(cap, dtype=torch.int32, device="cuda") for _ in range(3))
     t = 0
-    while t < 34:
+    while t < last:
         seeds = sched.seeds(t)
         if t in checked:
             pre = gm.state()[:3]
             log("full size t=%d: checked step" % t)
             res = gm.sample(to_dev(seeds), bbs[0])
             _check_step("t=%d" % t, gm, bbs[0], res, seeds, t, w, g, local, store_np, pre, rng)
-            if t == 32:
+            if t == round_t:
                 sid, se, sa, _ = gm.state()
                 k = gm.evict_step((ev, sl, rp))
                 E = np.nonzero(se < np.float32(gm.alpha))[0]
@@ -145,13 +156,14 @@ def test_papers_share_full_size():
                 rows = gm.buffer_rows()
                 probe = rng.choice(cap, size=20000, replace=False)
                 assert np.array_equal(rows[probe], store_np[sid2[probe]])
-                log("round t=32: %d slots evicted and refilled" % k)
+                log("round t=%d: %d slots evicted and refilled" % (t, k))
             else:
-                assert gm.evict_step() == 0
+                k = gm.evict_step()
+                assert k == 0 or (t > 0 and t % w.delta == 0)
             t += 1
             continue
         # look-ahead run up to the next checked step
-        stop = min(x for x in checked | {34} if x > t)
+        stop = min(x for x in checked | {last} if x > t)
         log("full size t=%d..%d: look-ahead" % (t, stop - 1))
         for u in range(t, stop + 1):
             if u < stop:
