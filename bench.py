@@ -35,7 +35,7 @@ def gather_traffic(rb_per_launch):
     import hashlib
     prof = os.path.join(ROOT, "profiles", "gather_hbm_cl111m_p64_hbm_counters.txt")
     src = open(os.path.join(ROOT, "paper_2410_22697_amd", "csrc", "buffer_kernels.hpp")).read()
-    a, b = src.find("__device__ __forceinline__ void gather_body"), src.find("// misses: pinned host store")
+    a, b = src.find("// ---------------------------------------------------------------- gather"), src.find("// misses: pinned host store")
     if not os.path.exists(prof) or a < 0 or b < 0:
         return None
     kv = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if l.startswith(("traffic_", "gather_source")))
@@ -65,37 +65,11 @@ def build_inputs(w, threads=None):
     return g, local, store, sched
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=192)
-    ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="cl111m_p64")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle baseline")
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--threads", type=int, default=None)
-    ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
-    ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
-    ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
-    ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
-    ap.add_argument("--copy-probe", action="store_true",
-                    help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (each partition's "
-              "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
-        sys.exit(2)
-
+def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False):
+    """One context over steps 0..warmup+steps-1 with look-ahead; the last
+    `steps` are timed. Returns the raw measurements."""
     import torch
-    import synth
     from paper_2410_22697_amd import Massive
-
-    w = synth.get(args.workload)
-    over = {k: v for k, v in (("delta", args.delta), ("gamma", args.gamma), ("buffer_pct", args.buffer_pct))
-            if v is not None}
-    if over:
-        w = w.with_(**over)
-    g, local, store, sched = build_inputs(w, args.threads)
     torch.cuda.set_device(0)
     t0 = time.time()
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
@@ -104,11 +78,11 @@ def main():
     init_s = time.time() - t0
     log("massive_init %.2fs: cap=%d alpha=%.6g" % (init_s, gm.cap, gm.alpha))
     bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
-    total = args.warmup + args.steps
+    total = warmup + steps
     seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
     torch.cuda.synchronize()
 
-    if args.copy_probe:
+    if copy_probe:
         a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
         b = torch.empty_like(a)
         torch.cuda.synchronize()
@@ -117,9 +91,10 @@ def main():
         log("copy probe: 256 MiB device-to-device copy done")
         del a, b
 
-    first_steps = []  # the first steps' outputs, checked against the oracle below
+    first_steps = []  # the first steps' outputs, checked against the oracle
+    stats = []        # per step: local, hits, misses, rows, host-link rows
 
-    def run(t0, t1, stats):
+    def run(t0, t1):
         """Steps t0..t1-1 with look-ahead: step t+1 is enqueued (after step t's
         round) before step t is waited for, so its sampling overlaps step t's
         host-link reads."""
@@ -136,64 +111,121 @@ def main():
                     nK = r.n[-1]
                     first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
                                         bb.feat[:nK].cpu().numpy().copy()))
-                if args.log_steps:
+                if log_steps:
                     log("step %d local %d hits %d misses %d rows %d" % (prev, r.local, r.hits, r.misses, r.n[-1]))
             prev = t
 
-    run(0, args.warmup, [])
-    log("warmup %d steps done" % args.warmup)
+    run(0, warmup)
+    log("warmup %d steps done" % warmup)
     r0, e0 = gm.counters()
-
+    f0 = gm.refilled_rows()
     gm.set_timing(True)
-    stats = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(args.warmup, total, stats)
+    run(warmup, total)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     tim = gm.timing()
     r1, e1 = gm.counters()
-    rounds, evicted = r1 - r0, e1 - e0
-    K = args.steps
-    mbps = K / elapsed
-    log("timed %d steps in %.3fs: %.1f minibatches/s, %d rounds, %d evicted" % (K, elapsed, mbps, rounds, evicted))
+    f1 = gm.refilled_rows()
+    out = dict(gm_cap=gm.cap, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
+               stats=np.array(stats, np.float64), tim=tim, rounds=r1 - r0, evicted=e1 - e0, refilled=f1 - f0,
+               first_steps=first_steps)
+    del bbs, seeds_dev
+    gm.close()
+    return out
 
-    rb = w.row_bytes
-    loc = np.array([s[0] for s in stats], np.float64)
-    hit = np.array([s[1] for s in stats], np.float64)
-    mis = np.array([s[2] for s in stats], np.float64)
+
+def summarize(w, res):
+    """Throughput, the gather against the HBM roofline, the host link, the hit rate."""
+    K, rb = res["steps"], w.row_bytes
+    st = res["stats"][res["warmup"]:]
+    loc, hit, mis, host_rows = st[:, 0], st[:, 1], st[:, 2], st[:, 4]
     hbm_rows = loc + hit
+    tim = res["tim"]
+    mbps = K / res["elapsed"]
     # gather_hbm algorithmic bytes: read + write each HBM-sourced row, plus its 8-byte list entry
     g_ms, g_calls = tim["gather_hbm"]
-    g_bytes_per_launch = float(np.mean(2 * hbm_rows * rb + 8 * hbm_rows))
+    g_bytes = float(np.mean(2 * hbm_rows * rb + 8 * hbm_rows))
     g_avg_s = g_ms / 1e3 / max(g_calls, 1)
-    g_gbps = g_bytes_per_launch / g_avg_s / 1e9
     m_ms, m_calls = tim["gather_miss"]
-    host_rows = np.array([s[4] for s in stats], np.float64)
     m_bytes = float(np.mean(host_rows * rb))
-    m_gbps = m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9
-    hit_rate = float(hit.sum() / max(hit.sum() + mis.sum(), 1))
-    rf_ms, rf_calls = tim["refill"]
-    log("host link per step: %.1f MB miss gather (%.1f MB of them hits on refilling slots), "
-        "%.1f MB refill (amortised)" % (m_bytes / 1e6, float(np.mean((host_rows - mis) * rb)) / 1e6,
-                                        evicted * rb / max(K, 1) / 1e6))
-    for name, (ms, calls) in tim.items():
+    refill_bytes = res["refilled"] * rb / max(K, 1)  # copied by refill chunks inside the timed region, per step
+    return dict(mbps=mbps, g_bytes=g_bytes, g_avg_s=g_avg_s, g_gbps=g_bytes / g_avg_s / 1e9,
+                m_bytes=m_bytes, m_avg_us=1e3 * m_ms / max(m_calls, 1),
+                m_gbps=m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9 if m_ms > 0 else 0.0,
+                hit_rate=float(hit.sum() / max(hit.sum() + mis.sum(), 1)),
+                pend_bytes=float(np.mean((host_rows - mis) * rb)), refill_bytes=refill_bytes,
+                evicted_bytes=res["evicted"] * rb / max(K, 1),
+                link_gbps=(float(host_rows.sum()) * rb + res["refilled"] * rb) / res["elapsed"] / 1e9,
+                remote_rows=float(np.mean(host_rows)) + res["refilled"] / max(K, 1),
+                halo_rows=float(np.mean(hit + mis)))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=192)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="cl111m_p64")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle baseline")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--threads", type=int, default=None)
+    ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
+    ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
+    ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
+    ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
+    ap.add_argument("--compare", action="store_true",
+                    help="the paper's comparison on the same inputs: no buffer (f = 0), prefetch without "
+                         "eviction (no round within the run) and prefetch with eviction; one JSON line each")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (each partition's "
+              "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import synth
+
+    w = synth.get(args.workload)
+    over = {k: v for k, v in (("delta", args.delta), ("gamma", args.gamma), ("buffer_pct", args.buffer_pct))
+            if v is not None}
+    if over:
+        w = w.with_(**over)
+    g, local, store, sched = build_inputs(w, args.threads)
+    if args.compare:
+        compare(w, g, local, store, sched, args)
+        return
+
+    res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe)
+    sm = summarize(w, res)
+    K, rb = args.steps, w.row_bytes
+    log("timed %d steps in %.3fs: %.1f minibatches/s, %d rounds, %d evicted" %
+        (K, res["elapsed"], sm["mbps"], res["rounds"], res["evicted"]))
+    log("host link per step: %.1f MB miss gather (%.1f MB of them hits on refilling slots, written through), "
+        "%.1f MB refill copied (%.1f MB evicted); %.1f GB/s over the link" %
+        (sm["m_bytes"] / 1e6, sm["pend_bytes"] / 1e6, sm["refill_bytes"] / 1e6, sm["evicted_bytes"] / 1e6,
+         sm["link_gbps"]))
+    for name, (ms, calls) in res["tim"].items():
         log("  %-13s %9.3f ms total, %5d launches, %.1f us avg" % (name, ms, calls, 1e3 * ms / max(calls, 1)))
     log("gather_hbm %.0f B/launch, %.1f us, %.1f GB/s (%.1f%% of HBM); miss fetch %.1f GB/s; hit rate %.3f" %
-        (g_bytes_per_launch, g_avg_s * 1e6, g_gbps, 100 * g_gbps / HBM_PEAK_GBPS, m_gbps, hit_rate))
+        (sm["g_bytes"], sm["g_avg_s"] * 1e6, sm["g_gbps"], 100 * sm["g_gbps"] / HBM_PEAK_GBPS, sm["m_gbps"],
+         sm["hit_rate"]))
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, first_steps)
+        cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, res["first_steps"])
 
+    g_gbps = sm["g_gbps"]
     out = {
         "metric": "sampled+gathered minibatches/s; gather GB/s (% HBM peak); halo buffer hit rate",
-        "value": round(mbps, 3),
+        "value": round(sm["mbps"], 3),
         "unit": "minibatches/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": round(1e3 * elapsed / K, 4),
+        "ms_per_step": round(1e3 * res["elapsed"] / K, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -202,23 +234,66 @@ def main():
         "config": {"workload": w.name, "nodes": w.n, "partitions": w.parts, "partition": 0,
                    "L": g.L, "H": g.H, "csr_entries": g.nnz, "batch": w.batch, "fanout": list(w.fanout),
                    "row_bytes": rb, "buffer_pct": w.buffer_pct, "gamma": w.gamma, "delta": w.delta,
-                   "cap": gm.cap, "steps_timed": [args.warmup, total - 1], "eviction_rounds": rounds,
-                   "evicted_rows": evicted, "lookahead": 1, "parallelism": "one partition on one GPU"},
+                   "cap": res["gm_cap"], "steps_timed": [args.warmup, args.warmup + K - 1],
+                   "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"], "lookahead": 1,
+                   "parallelism": "one partition on one GPU"},
         "gather_GBps": round(g_gbps, 1),
         "gather_frac_hbm": round(g_gbps / HBM_PEAK_GBPS, 4),
-        "hit_rate": round(hit_rate, 4),
+        "hit_rate": round(sm["hit_rate"], 4),
         "roofline": {"bound": "hbm", "kernel": "gather_hbm", "achieved": round(g_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(g_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": gather_traffic(g_bytes_per_launch) if w.name == "cl111m_p64" else None,
-                     "bytes_per_launch": round(g_bytes_per_launch), "avg_us": round(g_avg_s * 1e6, 2)},
-        "host_link": {"kernel": "gather_miss", "achieved": round(m_gbps, 2), "peak": PCIE_PEAK_GBPS,
-                      "unit": "GB/s", "bytes_per_launch": round(m_bytes),
-                      "avg_us": round(1e3 * m_ms / max(m_calls, 1), 2)},
-        "phase_ms_per_step": {k: round(v[0] / K, 4) for k, v in tim.items()},
-        "init_s": round(init_s, 3),
+                     "traffic": gather_traffic(sm["g_bytes"]) if w.name == "cl111m_p64" else None,
+                     "bytes_per_launch": round(sm["g_bytes"]), "avg_us": round(sm["g_avg_s"] * 1e6, 2)},
+        "host_link": {"kernel": "gather_miss", "achieved": round(sm["m_gbps"], 2), "peak": PCIE_PEAK_GBPS,
+                      "unit": "GB/s", "bytes_per_launch": round(sm["m_bytes"]),
+                      "avg_us": round(sm["m_avg_us"], 2),
+                      "refill_bytes_per_step": round(sm["refill_bytes"]),
+                      "link_GBps_whole_run": round(sm["link_gbps"], 2)},
+        "phase_ms_per_step": {k: round(v[0] / K, 4) for k, v in res["tim"].items()},
+        "init_s": round(res["init_s"], 3),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def compare(w, g, local, store, sched, args):
+    """The paper's comparison (Section V) on one partition's share: no buffer
+    (every halo row over the link, the baseline without prefetching), prefetch
+    without eviction (the initial degree-ranked buffer kept for the whole run)
+    and prefetch with eviction. Same graph, features and seed schedule; each
+    mode from a fresh context, over the same steps."""
+    total = args.warmup + args.steps
+    modes = [("no_buffer", w.with_(buffer_pct=0)),
+             ("static", w.with_(delta=total + 1)),   # no round within the run
+             ("eviction", w)]
+    base = None
+    for name, wm in modes:
+        log("mode %s: f=%d%% delta=%d gamma=%g" % (name, wm.buffer_pct, wm.delta, wm.gamma))
+        res = run_context(wm, g, local, store, sched, args.warmup, args.steps)
+        sm = summarize(wm, res)
+        if base is None:
+            base = sm
+        st = res["stats"]
+        series = (st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)).round(4).tolist()  # per step, from step 0
+        out = {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": name,
+               "value": round(sm["mbps"], 3), "unit": "minibatches/s", "n_gpus": 1, "steps": args.steps,
+               "warmup": args.warmup, "dtype": "f32" if wm.dtype == "f32" else "bf16",
+               "config": {"workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
+                          "cap": res["gm_cap"], "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"]},
+               "init_s": round(res["init_s"], 3), "init_rows_over_link": res["gm_cap"],
+               "hit_rate": round(sm["hit_rate"], 4),
+               "halo_rows_per_step": round(sm["halo_rows"], 1),
+               "remote_rows_per_step": round(sm["remote_rows"], 1),
+               "remote_rows_vs_no_buffer": round(sm["remote_rows"] / max(base["remote_rows"], 1e-9), 4),
+               "miss_gather_rows_per_step": round(sm["m_bytes"] / wm.row_bytes, 1),
+               "refill_rows_per_step": round(sm["refill_bytes"] / wm.row_bytes, 1),
+               "link_GBps_whole_run": round(sm["link_gbps"], 2),
+               "speedup_vs_no_buffer": round(sm["mbps"] / base["mbps"], 4),
+               "gather_frac_hbm": round(sm["g_gbps"] / HBM_PEAK_GBPS, 4),
+               "hit_rate_per_step": series}
+        log("mode %s: %.1f minibatches/s, hit rate %.3f, %.0f remote rows per step (%.3f of no buffer)" %
+            (name, sm["mbps"], sm["hit_rate"], sm["remote_rows"], out["remote_rows_vs_no_buffer"]))
+        print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):

@@ -154,8 +154,12 @@ int massive_batch_wait(massive_ctx* ctx, massive_batch* io);
 int massive_evict_step(massive_ctx* ctx, int32_t* evicted, int32_t* slots, int32_t* replaced,
                        int64_t* k_out);
 
-/* Totals since init: rounds that evicted at least one slot, slots evicted. */
-int massive_get_counters(massive_ctx* ctx, int64_t* rounds, int64_t* evicted);
+/* Totals since init (each pointer may be NULL): rounds that evicted at least
+ * one slot, slots evicted, and rows the refill copied over the host link
+ * (including the initial fill of the buffer; a replacement whose row a miss
+ * gather already wrote into its slot is not copied again). Waits for the
+ * refill chunks launched so far. */
+int massive_get_counters(massive_ctx* ctx, int64_t* rounds, int64_t* evicted, int64_t* refilled);
 
 /* Host copies of the prefetcher state (each pointer may be NULL):
  * slot_id[cap] halo id per slot, S_E[cap], S_A[H], steps sampled so far. */

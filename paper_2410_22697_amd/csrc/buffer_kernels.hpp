@@ -69,6 +69,7 @@ struct ClassifyArgs {
   uint8_t* mask;
   int2* hbm_list;
   int2* miss_list;
+  int32_t* miss_slot;         // per miss-list entry: the slot of a pending hit, else -1
   const int32_t* slot_round;  // round that last refilled each slot
   const int32_t* landed;      // round whose refill row has landed in each slot
   int32_t pend_round;         // refill of this round may still be in flight (-1: none)
@@ -89,7 +90,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   const int64_t tile = (int64_t)kClsNT * kClsItems;
   for (int64_t b0 = (int64_t)blockIdx.x * tile; b0 < n; b0 += (int64_t)gridDim.x * tile) {
     int cls[kClsItems];
-    int32_t src[kClsItems];
+    int32_t src[kClsItems], wslot[kClsItems];
     int ch = 0, cm = 0, cl = 0, cp = 0;  // hbm list, host list, local, pending hits
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
@@ -97,6 +98,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
       const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
       cls[it] = -1;
       src[it] = 0;
+      wslot[it] = -1;
       if (i < n) {
         const int32_t v = a.nodes[i];
         a.pos_of[v] = -1;
@@ -116,6 +118,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
                 __hip_atomic_load(&a.landed[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.pend_round) {
               cls[it] = 3;
               src[it] = h;
+              wslot[it] = slot;
             }
           } else {
             cls[it] = 2;
@@ -164,7 +167,10 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
       const uint64_t mh = ballot(cls[it] == 0 || cls[it] == 1);
       const uint64_t mm = ballot(cls[it] >= 2);
       if (cls[it] == 0 || cls[it] == 1) a.hbm_list[oh + lanes_below(mh)] = make_int2((int32_t)i, src[it]);
-      else if (cls[it] >= 2) a.miss_list[om + lanes_below(mm)] = make_int2((int32_t)i, src[it]);
+      else if (cls[it] >= 2) {
+        a.miss_list[om + lanes_below(mm)] = make_int2((int32_t)i, src[it]);
+        a.miss_slot[om + lanes_below(mm)] = wslot[it];
+      }
       oh += __popcll(mh);
       om += __popcll(mm);
     }
@@ -175,83 +181,143 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
 // ---------------------------------------------------------------- gather
 // dst row list[x].x <- src row list[x].y, as a bit copy of row_bytes. The
 // (row, chunk) work is flattened so every lane moves one vector per chunk
-// whatever the row size; four chunks are in flight per lane.
+// whatever the row size. Each lane takes U chunks per pass: first every list
+// entry, then every row load, then the stores, so all U loads of a lane are in
+// flight together. No load may sit behind a branch (the compiler would sink it
+// into the predicated store and wait for it there): in the last pass a lane
+// past the end re-reads its first chunk, or, where re-reading costs host-link
+// bytes, a dummy device row; the loaded values are pinned with an empty asm
+// before the predicated stores.
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
-template <typename V>
+// chunk cc of the flattened space -> (list entry, byte offset in the row);
+// ONE: one chunk per row (no division)
+template <typename V, bool ONE>
+__device__ __forceinline__ void chunk_of(uint64_t cc, uint32_t cpr, uint64_t magic, uint64_t& task,
+                                         uint64_t& off) {
+  task = ONE ? cc : __umul64hi(cc, magic);
+  off = (cc - task * cpr) * sizeof(V);
+}
+
+template <typename V, bool ONE, int U>
 __device__ __forceinline__ void gather_body(const int2* __restrict__ list, const int64_t* __restrict__ count,
                                             const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, int64_t rb,
                                             uint32_t cpr, uint64_t magic) {
   const uint64_t n = (uint64_t)*count;
   const uint64_t total = n * cpr;
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  auto split = [&](uint64_t cc, uint64_t& task, uint32_t& ch) {
-    task = cpr == 1 ? cc : __umul64hi(cc, magic);
-    ch = (uint32_t)(cc - task * cpr);
-  };
-  for (; c + 3 * stride < total; c += 4 * stride) {
-    V v[4];
-    int2 e[4];
-    uint32_t ch[4];
+  for (uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total; c += U * stride) {
+    uint64_t task[U], off[U];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      uint64_t task;
-      split(c + u * stride, task, ch[u]);
-      e[u] = list[task];
-      v[u] = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e[u].y * rb + (uint64_t)ch[u] * sizeof(V));
+    for (int u = 0; u < U; ++u) {
+      const uint64_t cc = c + u * stride;
+      chunk_of<V, ONE>(cc < total ? cc : c, cpr, magic, task[u], off[u]);
     }
+    int2 e[U];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e[u].x * rb +
-                                                             (uint64_t)ch[u] * sizeof(V)));
-  }
-  for (; c < total; c += stride) {
-    uint64_t task;
-    uint32_t ch;
-    split(c, task, ch);
-    const int2 e = list[task];
-    const V v = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e.y * rb + (uint64_t)ch * sizeof(V));
-    __builtin_nontemporal_store(v, reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e.x * rb + (uint64_t)ch * sizeof(V)));
+    for (int u = 0; u < U; ++u) e[u] = list[task[u]];
+    V v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      v[u] = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e[u].y * rb + off[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) asm volatile("" : "+v"(v[u]));
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c + u * stride < total)
+        __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e[u].x * rb + off[u]));
   }
 }
 
 // local rows and buffer hits: HBM slab -> output rows
-template <typename V>
+template <typename V, bool ONE>
 __global__ __launch_bounds__(256) void k_gather_hbm(const int2* __restrict__ list, const int64_t* __restrict__ count,
                                                     const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
                                                     int64_t rb, uint32_t cpr, uint64_t magic) {
-  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+  gather_body<V, ONE, 4>(list, count, src, dst, rb, cpr, magic);
 }
-// misses: pinned host store (over the host link) -> output rows
-template <typename V>
-__global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int64_t* __restrict__ count,
-                                                     const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                                     int64_t rb, uint32_t cpr, uint64_t magic) {
-  gather_body<V>(list, count, src, dst, rb, cpr, magic);
+// misses: pinned host store (over the host link) -> output rows. The list
+// also holds the hits on slots whose refill had not landed when the step was
+// classified; such a row is written into its buffer slot too (wslot >= 0), so
+// a replacement row crosses the link once, together with the misses (the
+// merged fetch of Algorithm 2). k_publish then marks those slots landed.
+// dummy: a device row of row_bytes that lanes past the end move onto itself.
+template <typename V, bool ONE>
+__global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int32_t* __restrict__ wslot,
+                                                     const int64_t* __restrict__ count, const uint8_t* __restrict__ src,
+                                                     uint8_t* __restrict__ dst, uint8_t* __restrict__ buf,
+                                                     uint8_t* __restrict__ dummy, int64_t rb, uint32_t cpr,
+                                                     uint64_t magic) {
+  constexpr int U = 4;
+  const uint64_t n = (uint64_t)*count;
+  const uint64_t total = n * cpr;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total; c += U * stride) {
+    uint64_t task[U], off[U];
+    bool in[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint64_t cc = c + u * stride;
+      in[u] = cc < total;
+      chunk_of<V, ONE>(in[u] ? cc : c, cpr, magic, task[u], off[u]);
+    }
+    int2 e[U];
+    int32_t ws[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      e[u] = list[task[u]];
+      ws[u] = wslot[task[u]];
+    }
+    V v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint8_t* p = in[u] ? src + (uint64_t)(uint32_t)e[u].y * rb + off[u] : dummy + off[u];
+      v[u] = *reinterpret_cast<const V*>(p);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint8_t* q = in[u] ? dst + (uint64_t)(uint32_t)e[u].x * rb + off[u] : dummy + off[u];
+      __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(q));
+      if (in[u] && ws[u] >= 0) *reinterpret_cast<V*>(buf + (uint64_t)(uint32_t)ws[u] * rb + off[u]) = v[u];
+    }
+  }
 }
+
+// After k_gather_miss (a kernel boundary: its row writes are complete): the
+// written-through slots are landed for round `round_id`.
+__global__ void k_publish(const int32_t* __restrict__ wslot, const int64_t* __restrict__ count,
+                          int32_t* __restrict__ landed, int64_t cap, int32_t round_id) {
+  const int64_t n = *count;
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t ws = wslot[x];
+    if (ws >= 0 && ws < cap) __hip_atomic_store(&landed[ws], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // Eviction refill: pinned host store -> buffer slots, row by row (G lanes
 // per row), in list order (replacements of highest S_A first), kRefillRows
-// rows in flight per lane group. Each batch of rows is then published:
-// release fence, then landed[slot] = round, which classify reads to serve hits
-// on those slots from HBM. (The fence waits for every store of the batch, so
-// batches are large.)
+// rows in flight per lane group. A row is copied unless its slot has landed
+// already (written through by a miss gather) or k_swap flagged the entry; a
+// row that is not copied moves the dummy device row onto itself instead, so
+// no load or store is behind a branch. Each batch of rows is then published:
+// release fence, then landed[slot] = round, which classify reads to serve
+// hits on those slots from HBM.
 constexpr int kRefillRows = 16;
 
 template <typename V>
 __global__ __launch_bounds__(256) void k_refill(const int2* __restrict__ list, const int64_t* __restrict__ count,
                                                 const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                                int64_t rb, uint32_t cpr, uint32_t G, int32_t L,
-                                                int32_t* __restrict__ landed, int32_t round_id, int32_t chunk,
-                                                int32_t nchunks) {
+                                                uint8_t* __restrict__ dummy, int64_t rb, uint32_t cpr, uint32_t G,
+                                                int32_t L, int32_t* __restrict__ landed, int32_t round_id,
+                                                int32_t chunk, int32_t nchunks, Counters* __restrict__ ctr) {
   // this launch refills fill-list rows [lo, hi): chunk `chunk` of `nchunks`
   const int64_t k = *count;
   const int64_t lo = k * chunk / nchunks, hi = k * (chunk + 1) / nchunks;
   const int64_t n = hi - lo;
   list += lo;
   const int lane = lane_id();
-  const int rpw = MS_WAVE / (int)G;  // row slots per wave
+  const int rpw = MS_WAVE / (int)G;  // row slots per wave (G divides the wave)
   const int sub = lane / (int)G, cl = lane % (int)G;
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / MS_WAVE;
   const int64_t nwaves = (int64_t)gridDim.x * blockDim.x / MS_WAVE;
@@ -262,24 +328,37 @@ __global__ __launch_bounds__(256) void k_refill(const int2* __restrict__ list, c
 #pragma unroll
     for (int u = 0; u < kRefillRows; ++u) {
       const int64_t r = base + (int64_t)u * rpw + sub;
-      ok[u] = sub < rpw && r < n;
-      e[u] = ok[u] ? list[r] : make_int2(0, 0);
-      ok[u] = ok[u] && e[u].x >= L && e[u].y >= 0;  // entries flagged inconsistent by k_swap are skipped
+      ok[u] = r < n;
+      e[u] = list[ok[u] ? r : base];
     }
+    int32_t lv[kRefillRows];
+#pragma unroll
+    for (int u = 0; u < kRefillRows; ++u) {
+      ok[u] = ok[u] && e[u].x >= L && e[u].y >= 0;  // entries flagged inconsistent by k_swap are skipped
+      lv[u] = __hip_atomic_load(&landed[ok[u] ? e[u].x - L : 0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+#pragma unroll
+    for (int u = 0; u < kRefillRows; ++u) ok[u] = ok[u] && lv[u] != round_id;
     for (uint32_t ch = cl; ch < cpr; ch += G) {
+      const uint64_t off = (uint64_t)ch * sizeof(V);
       V v[kRefillRows];
 #pragma unroll
       for (int u = 0; u < kRefillRows; ++u)
-        if (ok[u]) v[u] = *reinterpret_cast<const V*>(src + (uint64_t)(uint32_t)e[u].y * rb + (uint64_t)ch * sizeof(V));
+        v[u] = *reinterpret_cast<const V*>((ok[u] ? src + (uint64_t)(uint32_t)e[u].y * rb : dummy) + off);
 #pragma unroll
       for (int u = 0; u < kRefillRows; ++u)
-        if (ok[u]) *reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e[u].x * rb + (uint64_t)ch * sizeof(V)) = v[u];
+        *reinterpret_cast<V*>((ok[u] ? dst + (uint64_t)(uint32_t)e[u].x * rb : dummy) + off) = v[u];
     }
     __threadfence();
     if (cl == 0) {
+      unsigned long long copied = 0;
 #pragma unroll
       for (int u = 0; u < kRefillRows; ++u)
-        if (ok[u]) __hip_atomic_store(&landed[e[u].x - L], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (ok[u]) {
+          __hip_atomic_store(&landed[e[u].x - L], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          copied += 1;
+        }
+      if (copied) atomicAdd((unsigned long long*)&ctr->refilled, copied);
     }
   }
 }

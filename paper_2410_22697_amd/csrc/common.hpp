@@ -115,6 +115,8 @@ struct Counters {
   int64_t evicted;         // slots evicted (= rows refilled)
   int32_t bad;             // some round produced inconsistent indices (never expected)
   int32_t pad;
+  int64_t refilled;        // rows the refill copied over the host link (slots
+                           // written through by a miss gather are not copied)
 };
 
 }  // namespace ms

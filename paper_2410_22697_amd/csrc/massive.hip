@@ -56,6 +56,7 @@ struct massive_ctx {
   int64_t W = 0;        // bitmap words
   int64_t pmax = 0;     // partials capacity
   int64_t sort_cap = 0; // radix sort capacity
+  int64_t hbm_blocks = 4096;  // grid bound of the HBM gather
   int64_t host_blocks = 16;   // grid of the miss gather (host link)
   int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
@@ -65,6 +66,7 @@ struct massive_ctx {
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
   // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
   hipEvent_t ev_hbm_done[2] = {}, ev_batch_done[2] = {};
+  hipEvent_t ev_miss_done[2] = {};  // the miss gather kernel alone (before its publish and mailbox copies)
   hipEvent_t ev_swap_done = nullptr, ev_refill_done = nullptr;
   // The refill of the last round is copied in chunks, one after each of the
   // next steps' HBM gathers (host-link reads never overlap an HBM gather).
@@ -100,6 +102,8 @@ struct massive_ctx {
   int32_t* d_part2 = nullptr;
   int2* d_hbm_list = nullptr;
   int2* d_miss_list[2] = {};          // by step parity (read by the side stream)
+  int32_t* d_miss_slot[2] = {};       // per miss-list entry: write-through slot or -1
+  uint8_t* d_dummy = nullptr;         // [row_bytes] row that idle copy lanes move onto itself
   int32_t* d_E = nullptr;
   int32_t* d_R = nullptr;
   int2* d_fill = nullptr;
@@ -246,34 +250,46 @@ enum GatherKind { kHbm, kMiss };
 // fabric that HBM traffic also needs).
 // With timing on, the dispatch itself is bracketed by hipExtLaunchKernelGGL's
 // start/stop events (no launch latency in the measured time).
+// The miss gather also takes the write-through slots (wslot) and the buffer
+// rows (buf) of the hits on slots still refilling.
 void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, const int2* list,
                    const int64_t* count, const uint8_t* src, uint8_t* dst, int64_t rb, int64_t max_rows,
-                   int64_t max_blocks) {
+                   int64_t max_blocks, const int32_t* wslot = nullptr, uint8_t* buf = nullptr) {
   hipEvent_t ea = nullptr, eb = nullptr;
   const bool timed = c->kernel_pair(&ea, &eb);
   int vec = 4;
-  if (rb % 16 == 0 && ((uintptr_t)src % 16) == 0 && ((uintptr_t)dst % 16) == 0)
+  const uintptr_t al = (uintptr_t)src | (uintptr_t)dst | (uintptr_t)buf;
+  if (rb % 16 == 0 && al % 16 == 0)
     vec = 16;
-  else if (rb % 8 == 0 && ((uintptr_t)src % 8) == 0 && ((uintptr_t)dst % 8) == 0)
+  else if (rb % 8 == 0 && al % 8 == 0)
     vec = 8;
   const uint32_t cpr = (uint32_t)(rb / vec);
   const uint64_t magic = cpr > 1 ? (~0ull) / cpr + 1 : 0;
   const int64_t chunks = std::max<int64_t>(max_rows, 1) * cpr;
   const unsigned grid = grid_for(chunks / 4, 256, max_blocks);
-#define MS_LAUNCH(K, V)                                                                          \
-  do {                                                                                           \
-    if (timed)                                                                                   \
-      hipExtLaunchKernelGGL(ms::K<V>, dim3(grid), dim3(256), 0, s, ea, eb, 0, list, count, src, dst, rb, cpr, \
-                            magic);                                                              \
-    else                                                                                         \
-      ms::K<V><<<grid, 256, 0, s>>>(list, count, src, dst, rb, cpr, magic);                      \
+#define MS_ONE(V, ONE)                                                                                         \
+  do {                                                                                                         \
+    if (kind == kHbm) {                                                                                        \
+      if (timed)                                                                                               \
+        hipExtLaunchKernelGGL(ms::k_gather_hbm<V, ONE>, dim3(grid), dim3(256), 0, s, ea, eb, 0, list, count, src, \
+                              dst, rb, cpr, magic);                                                            \
+      else                                                                                                     \
+        ms::k_gather_hbm<V, ONE><<<grid, 256, 0, s>>>(list, count, src, dst, rb, cpr, magic);                  \
+    } else {                                                                                                   \
+      if (timed)                                                                                               \
+        hipExtLaunchKernelGGL(ms::k_gather_miss<V, ONE>, dim3(grid), dim3(256), 0, s, ea, eb, 0, list, wslot,  \
+                              count, src, dst, buf, c->d_dummy, rb, cpr, magic);                              \
+      else                                                                                                     \
+        ms::k_gather_miss<V, ONE><<<grid, 256, 0, s>>>(list, wslot, count, src, dst, buf, c->d_dummy, rb, cpr, \
+                                                       magic);                                                 \
+    }                                                                                                          \
   } while (0)
-#define MS_KIND(V)                         \
-  do {                                     \
-    if (kind == kHbm)                      \
-      MS_LAUNCH(k_gather_hbm, V);          \
-    else                                   \
-      MS_LAUNCH(k_gather_miss, V);         \
+#define MS_KIND(V)          \
+  do {                      \
+    if (cpr == 1)           \
+      MS_ONE(V, true);      \
+    else                    \
+      MS_ONE(V, false);     \
   } while (0)
   if (vec == 16)
     MS_KIND(ms::v4u);
@@ -282,7 +298,7 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
   else
     MS_KIND(unsigned int);
 #undef MS_KIND
-#undef MS_LAUNCH
+#undef MS_ONE
   if (timed) c->pending.push_back({ea, eb, group});
 }
 
@@ -309,10 +325,10 @@ void launch_refill(massive_ctx* c, hipStream_t s, const int64_t* count, int64_t 
   do {                                                                                                        \
     if (timed)                                                                                                \
       hipExtLaunchKernelGGL(ms::k_refill<V>, dim3(grid), dim3(256), 0, s, ea, eb, 0, (const int2*)c->d_fill, count, \
-                            src, dst, rb, cpr, G, c->L, c->d_landed, round_id, chunk, nchunks);               \
+                            src, dst, c->d_dummy, rb, cpr, G, c->L, c->d_landed, round_id, chunk, nchunks, c->d_ctr); \
     else                                                                                                      \
-      ms::k_refill<V><<<grid, 256, 0, s>>>(c->d_fill, count, src, dst, rb, cpr, G, c->L, c->d_landed, round_id, \
-                                           chunk, nchunks);                                                  \
+      ms::k_refill<V><<<grid, 256, 0, s>>>(c->d_fill, count, src, dst, c->d_dummy, rb, cpr, G, c->L, c->d_landed, round_id, \
+                                           chunk, nchunks, c->d_ctr);                                        \
   } while (0)
   if (vec == 16)
     MS_RF(ms::v4u);
@@ -347,7 +363,8 @@ void free_ctx(massive_ctx* c) {
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
-                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_E, c->d_R,
+                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_miss_slot[0],
+                 c->d_miss_slot[1], c->d_dummy, c->d_E, c->d_R,
                  c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
@@ -357,6 +374,7 @@ void free_ctx(massive_ctx* c) {
   if (c->h_bad) (void)hipHostFree(c->h_bad);
   if (c->h_ctr) (void)hipHostFree(c->h_ctr);
   for (hipEvent_t e : {c->ev_hbm_done[0], c->ev_hbm_done[1], c->ev_batch_done[0], c->ev_batch_done[1],
+                       c->ev_miss_done[0], c->ev_miss_done[1],
                        c->ev_swap_done, c->ev_refill_done})
     if (e) (void)hipEventDestroy(e);
   for (auto& r : c->pending) {
@@ -400,6 +418,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
     c->mu32[k] = mu * 4294967296.0;
   }
 
+  if (const char* e = getenv("MASSIVE_HBM_BLOCKS")) c->hbm_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_REFILL_BLOCKS")) c->refill_blocks = std::max(1, atoi(e));
   c->refill_chunks = std::min<int32_t>(a->delta, 32);
@@ -409,6 +428,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
   for (hipEvent_t* e : {&c->ev_hbm_done[0], &c->ev_hbm_done[1], &c->ev_batch_done[0], &c->ev_batch_done[1],
+                        &c->ev_miss_done[0], &c->ev_miss_done[1],
                         &c->ev_swap_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
 
@@ -447,6 +467,9 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_hbm_list, R * 8);
   CKA(c->d_miss_list[0], R * 8);
   CKA(c->d_miss_list[1], R * 8);
+  CKA(c->d_miss_slot[0], R * 4);
+  CKA(c->d_miss_slot[1], R * 4);
+  CKA(c->d_dummy, std::max<int64_t>(c->rb, 16));
   CKA(c->d_E, cap * 4);
   CKA(c->d_R, cap * 4);
   CKA(c->d_fill, cap * 8);
@@ -515,6 +538,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   for (int i = 0; i < 2; ++i) {
     CK(hipEventRecord(c->ev_hbm_done[i], s));
     CK(hipEventRecord(c->ev_batch_done[i], c->s_miss));
+    CK(hipEventRecord(c->ev_miss_done[i], c->s_miss));
   }
   CK(hipGetLastError());
   CK(hipStreamSynchronize(s));
@@ -682,6 +706,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ca.mask = io->mask;
     ca.hbm_list = c->d_hbm_list;
     ca.miss_list = miss_list;
+    ca.miss_slot = c->d_miss_slot[slot];
     ca.slot_round = c->d_slot_round;
     ca.landed = c->d_landed;
     ca.pend_round = pend;
@@ -693,18 +718,27 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   // whatever the main stream does next.
   // no host-link reads while the HBM gather runs: the previous step's miss
   // gather and the last refill chunk finish first
-  CK(hipStreamWaitEvent(s, c->ev_batch_done[slot ^ 1], 0));
+  CK(hipStreamWaitEvent(s, c->ev_miss_done[slot ^ 1], 0));
   if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
-  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K], 8192);
+  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
+                c->hbm_blocks);
   CK(hipEventRecord(c->ev_hbm_done[slot], s));
   {
     int rc = launch_refill_chunks(c, 1, c->ev_hbm_done[slot]);
     if (rc != MASSIVE_OK) return rc;
   }
   CK(hipStreamWaitEvent(c->s_miss, c->ev_hbm_done[slot], 0));
-  if (c->H > 0)
+  if (c->H > 0) {
     launch_gather(c, 3, kMiss, c->s_miss, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
-                  c->host_blocks);
+                  c->host_blocks, c->d_miss_slot[slot], c->d_slab + (int64_t)c->L * c->rb);
+  }
+  CK(hipEventRecord(c->ev_miss_done[slot], c->s_miss));
+  if (c->H > 0) {
+    // rows written through into their slots are landed from here on
+    if (pend >= 0)
+      ms::k_publish<<<grid_for(nb[c->K], 256, 1024), 256, 0, c->s_miss>>>(c->d_miss_slot[slot], &sz->n_miss,
+                                                                          c->d_landed, c->cap, pend);
+  }
   CK(hipMemcpyAsync(c->h_sz + slot, sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, c->s_miss));
   CK(hipMemcpyAsync(c->h_bad + slot, &c->d_ctr->bad, sizeof(int32_t), hipMemcpyDeviceToHost, c->s_miss));
   CK(hipEventRecord(c->ev_batch_done[slot], c->s_miss));
@@ -830,6 +864,9 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   // the refill is copied in chunks after the next steps' HBM gathers
   CK(hipEventRecord(c->ev_swap_done, s));
   CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
+  // the last step's miss gather may still write rows of the previous round's
+  // replacements into slots this round reassigns: the new refill comes after it
+  CK(hipStreamWaitEvent(c->s_copy, c->ev_batch_done[tl & 1], 0));
   c->chunks_left = c->refill_chunks;
   c->round_pending_rows = true;
   CK(hipGetLastError());
@@ -846,12 +883,14 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   return MASSIVE_OK;
 }
 
-int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted) {
+int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted, int64_t* refilled) {
   if (!c) return MASSIVE_EINVAL;
+  CK(hipStreamSynchronize(c->s_copy));  // refill chunks launched so far
   CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, c->s_main));
   CK(hipStreamSynchronize(c->s_main));
   if (rounds) *rounds = c->h_ctr->rounds;
   if (evicted) *evicted = c->h_ctr->evicted;
+  if (refilled) *refilled = c->h_ctr->refilled;
   return MASSIVE_OK;
 }
 
@@ -879,6 +918,7 @@ int massive_get_buffer_rows(massive_ctx* c, void* out) {
     if (rc != MASSIVE_OK) return rc;
   }
   if (c->refill_inflight) CK(hipStreamWaitEvent(c->s_main, c->ev_refill_done, 0));
+  CK(hipStreamSynchronize(c->s_miss));  // rows written through by miss gathers
   if (c->cap)
     CK(hipMemcpyAsync(out, c->d_slab + (int64_t)c->L * c->rb, c->cap * c->rb, hipMemcpyDeviceToHost, c->s_main));
   CK(hipStreamSynchronize(c->s_main));

@@ -71,7 +71,7 @@ def load():
     lib.massive_sample_async.argtypes = [vp, vp, i32, P(Batch)]
     lib.massive_batch_wait.argtypes = [vp, P(Batch)]
     lib.massive_evict_step.argtypes = [vp, vp, vp, vp, vp]
-    lib.massive_get_counters.argtypes = [vp, P(i64), P(i64)]
+    lib.massive_get_counters.argtypes = [vp, P(i64), P(i64), P(i64)]
     lib.massive_get_state.argtypes = [vp, vp, vp, vp, P(i64)]
     lib.massive_get_buffer_rows.argtypes = [vp, vp]
     lib.massive_info.argtypes = [vp, P(i64), P(ctypes.c_float)]
@@ -245,9 +245,17 @@ class Massive:
         return int(k.value)
 
     def counters(self):
+        """(rounds that evicted, slots evicted) since init."""
         r, e = ctypes.c_int64(), ctypes.c_int64()
-        self._check(self._lib.massive_get_counters(self._h, ctypes.byref(r), ctypes.byref(e)))
+        self._check(self._lib.massive_get_counters(self._h, ctypes.byref(r), ctypes.byref(e), None))
         return int(r.value), int(e.value)
+
+    def refilled_rows(self):
+        """Rows the refill has copied over the host link since init (the
+        initial fill included)."""
+        f = ctypes.c_int64()
+        self._check(self._lib.massive_get_counters(self._h, None, None, ctypes.byref(f)))
+        return int(f.value)
 
     def state(self):
         sid = np.zeros(max(self.cap, 1), np.int32)

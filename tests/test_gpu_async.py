@@ -3,7 +3,8 @@ in flight and eviction rounds enqueued without waiting, against the oracle
 run step by step. With a short eviction interval on the products-sized graph
 the refills (hundreds of thousands of rows over the host link) are still in
 flight when the next steps classify, so hits on refilled slots are served
-from the host store; the outputs must not change."""
+from the host store and written through into their slots (the refill then
+skips them); the outputs and the buffer rows must not change."""
 import numpy as np
 import pytest
 
@@ -30,9 +31,11 @@ def run_lookahead(name, prob, seeds_of, steps):
             for _ in range(steps)]
     seeds_dev = [to_dev(seeds_of(t)) for t in range(steps)]
     rounds_o, evicted_o = [], 0
+    pending = []
 
     def check(t):
         res = gm.wait(bbs[t % 2])
+        pending.append(res.host_rows - res.misses)
         st = orc.sample(seeds_of(t))
         compare_step("%s t=%d" % (name, t), st, res, bbs[t % 2], K)
         ro = orc.evict_step()
@@ -57,18 +60,22 @@ def run_lookahead(name, prob, seeds_of, steps):
     compare_state(name + " end", orc, gm)
     assert np.array_equal(gm.buffer_rows(), orc.buffer_rows())
     assert gm.counters() == (n_rounds, evicted_o)
-    log("%s: %d steps, %d rounds, %d evicted" % (name, steps, n_rounds, evicted_o))
-    return n_rounds
+    # the refill copies each replacement at most once, and none a miss gather wrote through
+    assert cap <= gm.refilled_rows() <= cap + evicted_o
+    log("%s: %d steps, %d rounds, %d evicted, pending hits per step %s" % (name, steps, n_rounds, evicted_o, pending))
+    assert min(pending) >= 0
+    return n_rounds, sum(pending)
 
 
 def test_lookahead_cl10k():
     prob, sched, w = workload_problem("cl10k", delta=3, gamma=0.8)
-    assert run_lookahead("async cl10k", prob, sched.seeds, 24) >= 3
+    assert run_lookahead("async cl10k", prob, sched.seeds, 24)[0] >= 3
 
 
 def test_lookahead_cl2m45_inflight_refills():
     prob, sched, w = workload_problem("cl2m45", delta=2)
-    assert run_lookahead("async cl2m45", prob, sched.seeds, 6) == 2
+    rounds, pending = run_lookahead("async cl2m45", prob, sched.seeds, 6)
+    assert rounds == 2 and pending > 0  # hits on refilling slots were written through
 
 
 def test_lookahead_rejects_a_third_batch():
