@@ -177,6 +177,10 @@ def main():
     ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the paper's parameter grid (f in 15/25/35/50 %%, gamma in 0.95/0.995/0.9995, delta in "
+                         "16..1024) on the same inputs, plus no buffer and one static run per f; one JSON line each")
+    ap.add_argument("--sweep-steps", type=int, default=1032, help="timed steps per sweep point (after 8 warm-up)")
     ap.add_argument("--compare", action="store_true",
                     help="the paper's comparison on the same inputs: no buffer (f = 0), prefetch without "
                          "eviction (no round within the run) and prefetch with eviction; one JSON line each")
@@ -196,6 +200,9 @@ def main():
     g, local, store, sched = build_inputs(w, args.threads)
     if args.compare:
         compare(w, g, local, store, sched, args)
+        return
+    if args.sweep:
+        sweep(w, g, local, store, sched, args)
         return
 
     res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe)
@@ -294,6 +301,42 @@ def compare(w, g, local, store, sched, args):
         log("mode %s: %.1f minibatches/s, hit rate %.3f, %.0f remote rows per step (%.3f of no buffer)" %
             (name, sm["mbps"], sm["hit_rate"], sm["remote_rows"], out["remote_rows_vs_no_buffer"]))
         print(json.dumps(out), flush=True)
+
+
+def sweep(w, g, local, store, sched, args):
+    """Section V-B's analysis of f, gamma and delta (Fig. 12-13) on one partition's share:
+    every point from a fresh context over the same steps and seed schedule,
+    against no buffer and against the static buffer of the same f."""
+    warm, steps = 8, args.sweep_steps
+    total = warm + steps
+
+    def point(kind, wm, base):
+        res = run_context(wm, g, local, store, sched, warm, steps)
+        sm = summarize(wm, res)
+        st = res["stats"]
+        hr = st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)
+        win = [round(float(x.mean()), 4) for x in np.array_split(hr, max(1, total // 64))]
+        out = {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": kind,
+               "workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
+               "steps": steps, "warmup": warm, "value": round(sm["mbps"], 3), "unit": "minibatches/s",
+               "hit_rate": round(sm["hit_rate"], 4), "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"],
+               "remote_rows_per_step": round(sm["remote_rows"], 1),
+               "remote_rows_vs_no_buffer": round(sm["remote_rows"] / base["remote_rows"], 4) if base else 1.0,
+               "speedup_vs_no_buffer": round(sm["mbps"] / base["mbps"], 4) if base else 1.0,
+               "evict_ms_per_round": round(res["tim"]["evict_round"][0] / max(res["tim"]["evict_round"][1], 1), 3),
+               "hit_rate_per_64_steps": win}
+        log("%-9s f=%2d%% gamma=%-6g delta=%-5d %8.1f mb/s  hit %.3f  remote rows %.0f (%.3f)  rounds %d" %
+            (kind, wm.buffer_pct, wm.gamma, wm.delta, sm["mbps"], sm["hit_rate"], sm["remote_rows"],
+             out["remote_rows_vs_no_buffer"], res["rounds"]))
+        print(json.dumps(out), flush=True)
+        return sm
+
+    base = point("no_buffer", w.with_(buffer_pct=0), None)
+    for f in (15, 25, 35, 50):
+        point("static", w.with_(buffer_pct=f, delta=total + 1), base)
+        for gamma in (0.95, 0.995, 0.9995):
+            for delta in (16, 32, 64, 128, 256, 512, 1024):
+                point("eviction", w.with_(buffer_pct=f, gamma=gamma, delta=delta), base)
 
 
 def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):

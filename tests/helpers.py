@@ -82,6 +82,9 @@ def workload_problem(name: str, **over) -> Tuple[Problem, "synth.Schedule", "syn
         _CACHE[name] = (g, lf, hs)
     g, lf, hs = _CACHE[name]
     w = w.with_(**over) if over else w
+    if (w.d, w.dtype) != (lf.shape[1], synth.get(name).dtype):  # other row sizes: features drawn afresh
+        lf = synth.features(g.local_gid, w.d, w.dtype, w.seed)
+        hs = synth.features(g.halo_gid, w.d, w.dtype, w.seed)
     prob = Problem(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, lf, hs, w.d, w.dtype,
                    w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
     sched = synth.Schedule(g.L, w.train_pct, w.batch, w.seed)

@@ -93,3 +93,15 @@ def test_lookahead_rejects_a_third_batch():
     assert ei.value.code == -5
     gm.wait(bbs[0])
     gm.wait(bbs[1])
+
+
+# Rows of 4, 8, 12, 16, 100 and 4000 bytes (fp32) and 4 and 100 bytes (bf16):
+# one-chunk rows, 4- and 8-byte vectors, and refill rows longer than a
+# wavefront; every step after a round has hits on refilling slots.
+@pytest.mark.parametrize("d,dtype", [(1, "f32"), (2, "f32"), (3, "f32"), (4, "f32"), (25, "f32"), (1000, "f32"),
+                                     (2, "bf16"), (50, "bf16")])
+def test_lookahead_row_sizes(d, dtype):
+    prob, sched, w = workload_problem("cl10k", delta=2, gamma=0.8, d=d, dtype=dtype)
+    assert w.row_bytes == d * (4 if dtype == "f32" else 2)
+    rounds, pending = run_lookahead("async cl10k d=%d %s" % (d, dtype), prob, sched.seeds, 10)
+    assert rounds >= 3 and pending > 0
