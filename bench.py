@@ -181,6 +181,9 @@ def main():
                     help="the paper's parameter grid (f in 15/25/35/50 %%, gamma in 0.95/0.995/0.9995, delta in "
                          "16..1024) on the same inputs, plus no buffer and one static run per f; one JSON line each")
     ap.add_argument("--sweep-steps", type=int, default=1032, help="timed steps per sweep point (after 8 warm-up)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="Alg. 1's look-ahead against a stand-in trainer on its own stream (Section IV-C): "
+                         "path alone, trainer alone, serial and overlapped steps per trainer size")
     ap.add_argument("--compare", action="store_true",
                     help="the paper's comparison on the same inputs: no buffer (f = 0), prefetch without "
                          "eviction (no round within the run) and prefetch with eviction; one JSON line each")
@@ -203,6 +206,9 @@ def main():
         return
     if args.sweep:
         sweep(w, g, local, store, sched, args)
+        return
+    if args.overlap:
+        overlap(w, g, local, store, sched, args)
         return
 
     res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe)
@@ -337,6 +343,126 @@ def sweep(w, g, local, store, sched, args):
         for gamma in (0.95, 0.995, 0.9995):
             for delta in (16, 32, 64, 128, 256, 512, 1024):
                 point("eviction", w.with_(buffer_pct=f, gamma=gamma, delta=delta), base)
+
+
+def overlap(w, g, local, store, sched, args):
+    """Alg. 1's look-ahead (Section IV-C, Eqs. 2-6): minibatch t+1 is prepared
+    while minibatch t trains. The trainer is a stand-in, a 2-layer MLP forward
+    and backward in fp32 over every gathered row, on a stream of its own (the
+    paper's DDP training is outside this path); its hidden size sets t_DDP.
+    Measured per step, in order on one context: the path alone with
+    look-ahead (t_Prepare), the trainer alone (t_DDP), the serial loop
+    (prepare, then train: Eq. 2) and the overlapped loop (Eq. 5)."""
+    import torch
+    from paper_2410_22697_amd import Massive
+    assert w.dtype == "f32", "the stand-in trainer reads fp32 rows"
+    torch.cuda.set_device(0)
+    gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
+                 w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
+    main = torch.cuda.current_stream()
+    consumer = torch.cuda.Stream()
+    bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
+    W = args.steps
+    hids = (256, 1024, 4096)
+    total = 8 + W + len(hids) * (2 * (8 + W))
+    seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
+    torch.cuda.synchronize()
+    state = {"t": 0, "ev": [None, None], "n": 0}
+
+    class Trainer:
+        def __init__(self, hid):
+            gen = torch.Generator(device="cuda").manual_seed(hid)
+            self.W1 = (torch.randn(w.d, hid, device="cuda", generator=gen) / w.d ** 0.5).requires_grad_()
+            self.W2 = (torch.randn(hid, 1, device="cuda", generator=gen) / hid ** 0.5).requires_grad_()
+
+        def step(self, feat, n):
+            x = feat[:n].view(torch.float32)
+            loss = (torch.relu(x @ self.W1) @ self.W2).square().mean()
+            loss.backward()
+            with torch.no_grad():
+                for p in (self.W1, self.W2):
+                    p -= 1e-6 * p.grad
+                    p.grad = None
+
+    def train(tr, slot, n):
+        with torch.cuda.stream(consumer):
+            tr.step(bbs[slot].feat, n)
+            e = torch.cuda.Event()
+            e.record(consumer)
+        state["ev"][slot] = e
+
+    def lookahead(steps, tr):
+        t0, prev = state["t"], None
+        for t in range(t0, t0 + steps + 1):
+            if t < t0 + steps:
+                slot = t % 2
+                if state["ev"][slot] is not None:
+                    main.wait_event(state["ev"][slot])  # the trainer has read this batch
+                gm.sample_async(seeds_dev[t], bbs[slot])
+                gm.evict_step(wait=False)
+            if prev is not None:
+                r = gm.wait(bbs[prev % 2])
+                state["n"] = r.n[-1]
+                if tr is not None:
+                    train(tr, prev % 2, r.n[-1])
+            prev = t
+        state["t"] = t0 + steps
+
+    def serial(steps, tr):
+        for t in range(state["t"], state["t"] + steps):
+            slot = t % 2
+            gm.sample_async(seeds_dev[t], bbs[slot])
+            gm.evict_step(wait=False)
+            r = gm.wait(bbs[slot])
+            train(tr, slot, r.n[-1])
+            consumer.synchronize()
+        state["t"] += steps
+
+    def timed(fn, *a):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn(*a)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / W
+
+    lookahead(8, None)
+    gm.set_timing(True)
+    t_prep = timed(lookahead, W, None)
+    tim = gm.timing()
+    ph = {k: v[0] / W for k, v in tim.items()}  # ms per step
+    eq3 = ph["sample_dedup"] + ph["classify"] + max(ph["gather_hbm"], ph["gather_miss"])
+    log("path alone: %.3f ms per step; Eq. 3 terms (ms/step) %s" % (1e3 * t_prep, {k: round(v, 3) for k, v in ph.items()}))
+    for hid in hids:
+        tr = Trainer(hid)
+        n, slot = state["n"], (state["t"] - 1) % 2
+        for _ in range(3):
+            train(tr, slot, n)
+        consumer.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(20):
+            train(tr, slot, n)
+        consumer.synchronize()
+        t_ddp = (time.perf_counter() - t0) / 20
+        serial(8, tr)
+        T_ser = timed(serial, W, tr)
+        lookahead(8, tr)
+        T_ovl = timed(lookahead, W, tr)
+        eff = (t_prep + t_ddp - T_ovl) / min(t_prep, t_ddp)
+        out = {"metric": "ms per minibatch, prepare overlapped with a stand-in trainer", "mode": "overlap",
+               "workload": w.name, "steps": W, "trainer": "2-layer MLP fwd+bwd fp32, hidden %d, %d rows" % (hid, n),
+               "t_prepare_ms": round(1e3 * t_prep, 4), "t_ddp_ms": round(1e3 * t_ddp, 4),
+               "T_serial_ms": round(1e3 * T_ser, 4), "T_overlap_ms": round(1e3 * T_ovl, 4),
+               "eq5_max_ms": round(1e3 * max(t_prep, t_ddp), 4),
+               "overlap_efficiency": round(min(1.0, max(0.0, eff)), 4),
+               "improvement_serial_over_overlap": round(T_ser / T_ovl, 4),
+               "eq3_terms_ms_per_step": {k: round(v, 4) for k, v in ph.items()},
+               "eq3_sum_ms": round(eq3, 4)}
+        log("hidden %d: t_DDP %.3f ms, serial %.3f ms, overlapped %.3f ms per step (max(t_Prepare, t_DDP) = %.3f), "
+            "overlap efficiency %.2f" % (hid, 1e3 * t_ddp, 1e3 * T_ser, 1e3 * T_ovl, 1e3 * max(t_prep, t_ddp), eff))
+        print(json.dumps(out), flush=True)
+    torch.cuda.synchronize()
+    del bbs
+    gm.close()
 
 
 def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):
