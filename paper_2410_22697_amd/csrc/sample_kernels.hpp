@@ -182,6 +182,42 @@ struct SampleArgs {
   int32_t* err;             // threshold search could not isolate a candidate set
 };
 
+// Philox4x32-10 with counter (q, v, t, hop) for every q of one row. Words 1-3
+// of the counter are the same across the row, so round 1's product of word 2
+// (t) and round 2's product of word 0 (which round 1 builds from t, v and the
+// key only) are computed once per row; the other rounds are the published
+// block function unchanged (see philox4x32_10).
+struct PhiloxRow {
+  uint32_t x1, y1;      // words 0 and 1 after round 1
+  uint32_t a2hi, a2lo;  // round 2's 64-bit product of word 0
+  uint32_t hop, k0, k1;
+  __device__ __forceinline__ PhiloxRow(uint32_t v, uint32_t t, uint32_t hop_, uint32_t key0, uint32_t key1)
+      : hop(hop_), k0(key0), k1(key1) {
+    const uint64_t b1 = (uint64_t)0xCD9E8D57u * t;
+    x1 = (uint32_t)(b1 >> 32) ^ v ^ key0;
+    y1 = (uint32_t)b1;
+    const uint64_t a2 = (uint64_t)0xD2511F53u * x1;
+    a2hi = (uint32_t)(a2 >> 32);
+    a2lo = (uint32_t)a2;
+  }
+  __device__ __forceinline__ uint4 operator()(uint32_t q) const {
+    const uint64_t a1 = (uint64_t)0xD2511F53u * q;  // round 1, word 0
+    const uint32_t z1 = (uint32_t)(a1 >> 32) ^ hop ^ k1, w1 = (uint32_t)a1;
+    uint32_t r0 = k0 + 0x9E3779B9u, r1 = k1 + 0xBB67AE85u;  // round 2's key
+    const uint64_t b2 = (uint64_t)0xCD9E8D57u * z1;
+    uint4 c = make_uint4((uint32_t)(b2 >> 32) ^ y1 ^ r0, (uint32_t)b2, a2hi ^ w1 ^ r1, a2lo);
+#pragma unroll
+    for (int r = 2; r < 10; ++r) {
+      r0 += 0x9E3779B9u;
+      r1 += 0xBB67AE85u;
+      const uint64_t a = (uint64_t)0xD2511F53u * c.x;
+      const uint64_t b = (uint64_t)0xCD9E8D57u * c.z;
+      c = make_uint4((uint32_t)(b >> 32) ^ c.y ^ r0, (uint32_t)b, (uint32_t)(a >> 32) ^ c.w ^ r1, (uint32_t)a);
+    }
+    return c;
+  }
+};
+
 __device__ __forceinline__ uint64_t first_tau(double mu32, int64_t d) {
   const double t = mu32 / (double)d + 1.0;
   return t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t;
@@ -274,19 +310,20 @@ __device__ __forceinline__ void wave_lds_sync() {
 __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) {
   __shared__ uint64_t cand[kSampleWaves][kCandCap];
   if (a.sz->status) return;
-  const int lane = lane_id(), wave = wave_id();
+  const int lane = lane_id(), wave = wave_uniform(wave_id());
   const int64_t w = (int64_t)blockIdx.x * kSampleWaves + wave;
   int64_t row;
   if (w < a.row_waves) {
     if (w >= a.sz->n_big[a.hop - 1]) return;
-    row = a.big_rows[w];
+    row = wave_uniform((int32_t)a.big_rows[w]);
   } else {
     row = w - a.row_waves;
     if (row >= a.sz->n[a.hop - 1]) return;
   }
-  const int32_t v = a.nodes[row];
-  const int64_t start = a.csr_indptr[v];
-  const int64_t d = a.csr_indptr[v + 1] - start;
+  // the row, its node and its extent are the same in every lane
+  const int32_t v = wave_uniform(a.nodes[row]);
+  const int64_t start = wave_uniform(a.csr_indptr[v]);
+  const int64_t d = wave_uniform(a.csr_indptr[v + 1]) - start;
   if (w >= a.row_waves && d > a.big_min) return;  // taken by a wave of the big list
   const int32_t fo = a.fo;
   int32_t* out = a.out + a.bptr[row];
@@ -301,32 +338,39 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) 
   int cnt = 0;
   bool fail = false;
   const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
+  const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
   for (int iter = 0; iter < 48 && !fail; ++iter) {
     cnt = 0;
     const uint32_t tm1 = (uint32_t)(ts.tau - 1);  // key < tau  <=>  key <= tau - 1
     for (uint32_t q0 = 0; 4 * q0 < d32; q0 += MS_WAVE) {
       const uint32_t q = q0 + lane;
-      const uint4 wv = philox4x32_10(make_uint4(q, (uint32_t)v, a.t, (uint32_t)a.hop), a.key0, a.key1);
-      bool take[4];
+      const uint4 wv = ph(q);
+      // lane masks of the keys below tau, position j = 4q + s (held as scalar
+      // masks: the usual iteration of a long row takes none)
+      uint64_t m0, m1, m2, m3;
       if (4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
-#pragma unroll
-        for (int s = 0; s < 4; ++s) take[s] = word_of(wv, s) <= tm1;
+        m0 = ballot(wv.x <= tm1);
+        m1 = ballot(wv.y <= tm1);
+        m2 = ballot(wv.z <= tm1);
+        m3 = ballot(wv.w <= tm1);
       } else {
-#pragma unroll
-        for (int s = 0; s < 4; ++s) take[s] = (4 * q + s < d32) && word_of(wv, s) <= tm1;
+        m0 = ballot(4 * q < d32 && wv.x <= tm1);
+        m1 = ballot(4 * q + 1 < d32 && wv.y <= tm1);
+        m2 = ballot(4 * q + 2 < d32 && wv.z <= tm1);
+        m3 = ballot(4 * q + 3 < d32 && wv.w <= tm1);
       }
-      if (!ballot(take[0] || take[1] || take[2] || take[3])) continue;  // usual case for long rows
-      uint64_t m[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) m[s] = ballot(take[s]);
-      int p = cnt + lanes_below(m[0]) + lanes_below(m[1]) + lanes_below(m[2]) + lanes_below(m[3]);
+      if (!(m0 | m1 | m2 | m3)) continue;
+      // candidates in ascending j: lower lanes first, then s within the lane
+      int p = cnt + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+      const uint64_t bit = 1ull << lane;
+      const uint64_t m[4] = {m0, m1, m2, m3};
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        if (take[s]) {
+        if (m[s] & bit) {
           if (p < kCandCap) c[p] = ((uint64_t)word_of(wv, s) << 32) | (4 * q + s);
           ++p;
         }
-      cnt += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+      cnt += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
     }
     if (ts.step(cnt, fo, kCandCap, &fail)) break;
   }
