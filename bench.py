@@ -93,6 +93,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
 
     first_steps = []  # the first steps' outputs, checked against the oracle
     stats = []        # per step: local, hits, misses, rows, host-link rows
+    sizes = []        # per step: frontier sizes n_0..n_K and sampled edges e_1..e_K
 
     def run(t0, t1):
         """Steps t0..t1-1 with look-ahead: step t+1 is enqueued (after step t's
@@ -106,13 +107,15 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
             if prev is not None:
                 r = gm.wait(bbs[prev % 2])
                 stats.append((r.local, r.hits, r.misses, r.n[-1], r.host_rows))
+                sizes.append((list(r.n), list(r.e)))
                 if prev < 2 and len(first_steps) == prev:
                     bb = bbs[prev % 2]
                     nK = r.n[-1]
                     first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
                                         bb.feat[:nK].cpu().numpy().copy()))
                 if log_steps:
-                    log("step %d local %d hits %d misses %d rows %d" % (prev, r.local, r.hits, r.misses, r.n[-1]))
+                    log("step %d local %d hits %d misses %d rows %d host %d" % (prev, r.local, r.hits, r.misses,
+                                                                                r.n[-1], r.host_rows))
             prev = t
 
     run(0, warmup)
@@ -128,12 +131,25 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     tim = gm.timing()
     r1, e1 = gm.counters()
     f1 = gm.refilled_rows()
-    out = dict(gm_cap=gm.cap, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
-               stats=np.array(stats, np.float64), tim=tim, rounds=r1 - r0, evicted=e1 - e0, refilled=f1 - f0,
-               first_steps=first_steps)
+    out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
+               stats=np.array(stats, np.float64), sizes=sizes, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
+               refilled=f1 - f0, first_steps=first_steps)
     del bbs, seeds_dev
     gm.close()
     return out
+
+
+def alg_hbm_bytes(n, e, loc, hit, mis, rb):
+    """HBM bytes one minibatch must move by the method's definition, whatever
+    the implementation: per hop, the frontier row's id and CSR offsets (16 B),
+    the selected ids, the block offsets and block entries, and ~12 B per
+    sampled edge for dedup/relabel; then ~13 B per input row to classify and
+    mark it, the local and buffer rows read and written, the miss rows
+    written, and 8 B of score traffic per halo row."""
+    b = 0
+    for k in range(len(e)):
+        b += 16 * n[k] + 4 * e[k] + 4 * (n[k] + 1) + 4 * e[k] + 12 * e[k]
+    return b + 13 * n[-1] + 2 * (loc + hit) * rb + mis * rb + 8 * (mis + hit)
 
 
 def summarize(w, res):
@@ -151,7 +167,12 @@ def summarize(w, res):
     m_ms, m_calls = tim["gather_miss"]
     m_bytes = float(np.mean(host_rows * rb))
     refill_bytes = res["refilled"] * rb / max(K, 1)  # copied by refill chunks inside the timed region, per step
-    return dict(mbps=mbps, g_bytes=g_bytes, g_avg_s=g_avg_s, g_gbps=g_bytes / g_avg_s / 1e9,
+    sz = res["sizes"][res["warmup"]:]
+    b_alg = float(np.mean([alg_hbm_bytes(n, e, l, h, m, rb) for (n, e), (l, h, m) in zip(sz, st[:, :3])]))
+    # eviction rounds, amortised: S_E/slot scans and S_A/rank scans, and the replacement rows written
+    b_alg += (res["rounds"] * (12 * res["gm_cap"] + 8 * res["H"]) + res["evicted"] * rb) / max(K, 1)
+    link_bytes = float(np.mean(host_rows * rb)) + refill_bytes
+    return dict(mbps=mbps, b_alg=b_alg, link_bytes=link_bytes, g_bytes=g_bytes, g_avg_s=g_avg_s, g_gbps=g_bytes / g_avg_s / 1e9,
                 m_bytes=m_bytes, m_avg_us=1e3 * m_ms / max(m_calls, 1),
                 m_gbps=m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9 if m_ms > 0 else 0.0,
                 hit_rate=float(hit.sum() / max(hit.sum() + mis.sum(), 1)),
@@ -262,6 +283,14 @@ def main():
                       "avg_us": round(sm["m_avg_us"], 2),
                       "refill_bytes_per_step": round(sm["refill_bytes"]),
                       "link_GBps_whole_run": round(sm["link_gbps"], 2)},
+        "minibatch_roofline": {"bound": "host link",
+                               "hbm_alg_bytes_per_step": round(sm["b_alg"]),
+                               "hbm_GBps": round(sm["mbps"] * sm["b_alg"] / 1e9, 1),
+                               "hbm_frac": round(sm["mbps"] * sm["b_alg"] / 1e9 / HBM_PEAK_GBPS, 4),
+                               "link_bytes_per_step": round(sm["link_bytes"]),
+                               "link_GBps": round(sm["mbps"] * sm["link_bytes"] / 1e9, 2),
+                               "link_peak_GBps": PCIE_PEAK_GBPS,
+                               "link_frac": round(sm["mbps"] * sm["link_bytes"] / 1e9 / PCIE_PEAK_GBPS, 4)},
         "phase_ms_per_step": {k: round(v[0] / K, 4) for k, v in res["tim"].items()},
         "init_s": round(res["init_s"], 3),
         "cpu_baseline": cpu,
