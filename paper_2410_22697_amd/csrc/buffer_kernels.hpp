@@ -419,19 +419,13 @@ __global__ __launch_bounds__(kScanNT) void k_evict_emit(const float* __restrict_
 }
 
 // |C| = number of unbuffered halo nodes (S_A >= 0).
-__global__ __launch_bounds__(256) void k_count_candidates(const float* __restrict__ S_A, int64_t H,
-                                                          int64_t* __restrict__ out) {
-  __shared__ int64_t lds[256 / MS_WAVE + 1];
-  int64_t c = 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x)
-    c += S_A[i] >= 0.0f;
-  c = block_sum<256>(c, lds);
-  if (threadIdx.x == 0 && c) atomicAdd((unsigned long long*)out, (unsigned long long)c);
-}
-
 // k' = min(|E|, |C|) on the device; sets the select and the E narrowing up.
-__global__ void k_round_setup(RoundState* __restrict__ rs, Counters* __restrict__ ctr) {
-  const int64_t k = rs->nE < rs->nC ? rs->nE : rs->nC;
+// |C| = H - cap always: a halo node has S_A = -1 exactly while it is buffered
+// (init, and the swap's S_A := -1 for a replacement) and S_A >= 0 otherwise
+// (misses only add to it; an evicted node gets its last S_E >= 0).
+__global__ void k_round_setup(RoundState* __restrict__ rs, Counters* __restrict__ ctr, int64_t nC) {
+  rs->nC = nC;
+  const int64_t k = rs->nE < nC ? rs->nE : nC;
   rs->k = k;
   rs->need = k;
   rs->prefix = 0;

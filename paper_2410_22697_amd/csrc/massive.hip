@@ -71,7 +71,7 @@ struct massive_ctx {
   // The refill of the last round is copied in chunks, one after each of the
   // next steps' HBM gathers (host-link reads never overlap an HBM gather).
   int32_t round_id = 0;          // rounds so far, as stamped in slot_round / landed
-  int32_t refill_chunks = 1;     // chunks per round: min(delta, 32), one per step of the interval
+  int32_t refill_chunks = 1;     // chunks per round: min(delta - 1, 32), one per step of the interval
   int32_t chunks_left = 0;       // chunks of round_id's refill not yet launched
   bool refill_inflight = false;  // a launched chunk may not have landed
   bool round_pending_rows = false;  // round_id's refill not fully landed (hits may need the host)
@@ -421,7 +421,9 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (const char* e = getenv("MASSIVE_HBM_BLOCKS")) c->hbm_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_REFILL_BLOCKS")) c->refill_blocks = std::max(1, atoi(e));
-  c->refill_chunks = std::min<int32_t>(a->delta, 32);
+  // one chunk after each of the next steps' HBM gathers, all launched before
+  // the step of the next round, so that round never waits for a chunk in flight
+  c->refill_chunks = std::max<int32_t>(1, std::min<int32_t>(a->delta - 1, 32));
   if (const char* e = getenv("MASSIVE_REFILL_CHUNKS")) c->refill_chunks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
   c->s_main = (hipStream_t)a->stream;
@@ -831,17 +833,20 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     const int64_t nbe = std::max<int64_t>(1, cdiv(cap, ms::kScanTile));
     ms::k_evict_count<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part, &rs->nE);
     ms::k_evict_emit<<<(unsigned)nbe, ms::kScanNT, 0, s>>>(c->d_S_E, cap, c->alpha, c->d_part, c->d_E);
-    ms::k_count_candidates<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, &rs->nC);
-    ms::k_round_setup<<<1, 1, 0, s>>>(rs, c->d_ctr);
-    // fewer candidates than evictions (only when f > 50%): keep the k' slots of
-    // smallest (S_E, rank); every kernel here sees zero elements otherwise
-    ms::k_esel_keys_lo<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, &rs->nE_sel, c->d_slot_id, c->d_rank_of, c->d_k0,
-                                                          c->d_v0);
-    sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
-    ms::k_esel_keys_hi<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->nE_sel, c->d_S_E, c->d_k0);
-    sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
-    ms::k_esel_keys_slot<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->k_sel, c->d_k0);
-    sort_u32(c, s, &rs->k_sel, 0, cap, c->d_E);
+    ms::k_round_setup<<<1, 1, 0, s>>>(rs, c->d_ctr, H - cap);
+    // fewer candidates than evictions: keep the k' slots of smallest (S_E,
+    // rank). With |C| = H - cap >= cap >= |E| (f <= 50%) it cannot happen and
+    // the narrowing is not launched; otherwise its kernels see zero elements
+    // in rounds where it does not happen.
+    if (cap > H - cap) {
+      ms::k_esel_keys_lo<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, &rs->nE_sel, c->d_slot_id, c->d_rank_of,
+                                                            c->d_k0, c->d_v0);
+      sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
+      ms::k_esel_keys_hi<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->nE_sel, c->d_S_E, c->d_k0);
+      sort_u32(c, s, &rs->nE_sel, 0, cap, nullptr);
+      ms::k_esel_keys_slot<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->k_sel, c->d_k0);
+      sort_u32(c, s, &rs->k_sel, 0, cap, c->d_E);
+    }
     ms::k_fill_gated<int32_t><<<grid_for(cap, 256), 256, 0, s>>>(c->d_R, cap, -1, &rs->k);
     // radix select of the k'-th candidate key, 8 bits per pass
     for (int shift = 24; shift >= 0; shift -= 8) {
