@@ -408,8 +408,13 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   c->pmax = std::max(cdiv(c->R, ms::kScanTile), cdiv(256 * cdiv(c->sort_cap, ms::kSortTile), ms::kScanTile));
   c->pmax = std::max<int64_t>(c->pmax, cdiv(c->W, ms::kScanTile)) + 8;
   // Eq. 1 with S_E at its initial value 1: alpha = gamma^delta in fp32 products
+  // (once a product no longer changes the value, e.g. at 0, the rest cannot)
   float al = 1.0f;
-  for (int32_t i = 0; i < a->delta; ++i) al = al * a->gamma;
+  for (int32_t i = 0; i < a->delta; ++i) {
+    const float next = al * a->gamma;
+    if (next == al) break;
+    al = next;
+  }
   c->alpha = al;
   // sampler: about fo + 3 sqrt(fo) + 3 keys survive the first threshold
   for (int k = 0; k < a->K; ++k) {

@@ -159,7 +159,9 @@ __global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, in
 // as they are written. Rows longer than big_min (listed by k_row_counts) get
 // the first waves of the grid, so that the longest rows start first.
 constexpr int kSampleWaves = 4;
-constexpr int kCandCap = 256;   // candidates per wave (LDS); also the largest fanout
+constexpr int kCandSlots = 5;                   // candidates per lane in the selection
+constexpr int kCandCap = kCandSlots * MS_WAVE;  // candidates per wave (LDS): 320, so the
+                                                // largest fanout (256) keeps 64 of slack for ties
 constexpr int64_t kBigRow = 2048;
 
 struct SampleArgs {
@@ -251,18 +253,18 @@ __device__ __forceinline__ void emit_id(int32_t* __restrict__ out, int p, int32_
   }
 }
 
-// Selection among cnt <= 256 candidates held in LDS in ascending j
+// Selection among cnt <= kCandCap candidates held in LDS in ascending j
 // (list[i] = key << 32 | j); writes the fo chosen neighbours to out in
 // ascending j. One wavefront; element i sits in slot i / 64 of lane i % 64.
 __device__ __forceinline__ void select_emit(const uint64_t* list, int cnt, int fo, uint64_t tau,
                                             const int32_t* __restrict__ nb, int32_t* __restrict__ out,
                                             const int32_t* __restrict__ pos_of, uint32_t* __restrict__ bits) {
   const int lane = lane_id();
-  const int S = (cnt + MS_WAVE - 1) / MS_WAVE;  // 1..4
-  uint32_t key[4], pos[4];
-  bool valid[4];
+  const int S = (cnt + MS_WAVE - 1) / MS_WAVE;  // 1..kCandSlots
+  uint32_t key[kCandSlots], pos[kCandSlots];
+  bool valid[kCandSlots];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < kCandSlots; ++s) {
     const int idx = s * MS_WAVE + lane;
     valid[s] = s < S && idx < cnt;
     const uint64_t e = valid[s] ? list[idx] : 0ull;
@@ -280,9 +282,9 @@ __device__ __forceinline__ void select_emit(const uint64_t* list, int cnt, int f
     if (c < fo) T = trial;
   }
   int n_lt = 0;
-  uint64_t lt[4], eq[4];
+  uint64_t lt[kCandSlots], eq[kCandSlots];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < kCandSlots; ++s) {
     lt[s] = ballot(valid[s] && key[s] < T);
     eq[s] = ballot(valid[s] && key[s] == T);
     n_lt += __popcll(lt[s]);
@@ -291,7 +293,7 @@ __device__ __forceinline__ void select_emit(const uint64_t* list, int cnt, int f
   int eq_before = 0;  // ties in earlier slots (all lanes)
   int p_before = 0;   // selected in earlier slots
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < kCandSlots; ++s) {
     const bool is_lt = (lt[s] >> lane) & 1ull, is_eq = (eq[s] >> lane) & 1ull;
     const bool sel = is_lt || (is_eq && eq_before + lanes_below(eq[s]) < need);
     const uint64_t sm = ballot(sel);

@@ -47,6 +47,44 @@ def test_init_error_path_without_gpu():
     assert not h.value
 
 
+_BAD = [("K", 0, b"K must"), ("K", 9, b"K must"), ("fanout0", 0, b"fanout"), ("fanout0", 257, b"fanout"),
+        ("buffer_pct", 101, b"buffer_pct"), ("buffer_pct", -1, b"buffer_pct"), ("gamma", 0.0, b"gamma"),
+        ("gamma", 1.5, b"gamma"), ("delta", 0, b"delta"), ("row_bytes", 6, b"row_bytes"),
+        ("row_bytes", 0, b"row_bytes"), ("L", -1, b"L >= 0")]
+
+
+@pytest.mark.parametrize("field,value,msg", _BAD)
+def test_init_rejects_each_bad_argument_without_gpu(field, value, msg):
+    """Every argument outside its documented range is rejected before any device call."""
+    import numpy as np
+    from paper_2410_22697_amd import massive
+    if not os.path.exists(massive.LIB_PATH):
+        pytest.skip("libmassive.so not built")
+    lib = massive.load()
+    L, H = 2, 1
+    indptr = np.array([0, 1, 2, 2], np.int64)
+    indices = np.array([1, 0], np.int32)
+    gid = np.zeros(H, np.int32)
+    deg = np.zeros(H, np.int64)
+    feat = np.zeros((L + H, 4), np.float32)
+    a = massive.InitArgs()
+    a.L, a.H = L, H
+    a.indptr, a.indices = indptr.ctypes.data, indices.ctypes.data
+    a.halo_gid, a.halo_degree = gid.ctypes.data, deg.ctypes.data
+    a.local_feat = feat.ctypes.data
+    a.halo_store = feat[L:].ctypes.data
+    a.row_bytes, a.K, a.buffer_pct, a.gamma, a.delta = 16, 2, 25, 0.9, 2
+    a.fanout[0], a.fanout[1] = 3, 2
+    if field == "fanout0":
+        a.fanout[0] = value
+    else:
+        setattr(a, field, value)
+    h = ctypes.c_void_p()
+    assert lib.massive_init(ctypes.byref(a), ctypes.byref(h)) == massive.EINVAL
+    assert msg in lib.massive_last_error(None), lib.massive_last_error(None)
+    assert not h.value
+
+
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     from paper_2410_22697_amd import massive
     monkeypatch.setattr(massive, "LIB_PATH", str(tmp_path / "absent.so"))
