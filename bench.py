@@ -526,7 +526,19 @@ def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):
     return {"value": round(steps / el, 4), "unit": "minibatches/s", "cores": 1, "kind": "oracle",
             "sample": "steps 0..%d of %s from init (single-threaded C oracle; %d steps compared bit-exact "
                       "with the GPU run)" % (steps - 1, w.name, checked),
-            "host_cpus": os.cpu_count()}
+            "phase_s_per_step": {k: round(float(v) / steps, 4) for k, v in
+                                 zip(("sample", "dedup", "classify", "score", "gather", "evict"), ph)},
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 if __name__ == "__main__":
