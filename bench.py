@@ -139,6 +139,33 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     return out
 
 
+def copy_reference(nbytes, reps=20, regions=8):
+    """GB/s of a plain contiguous device-to-device copy (torch copy_) that
+    reads nbytes/2 and writes nbytes/2, as the gather does per launch: the
+    practical ceiling for a copy of this size on this GPU. Consecutive copies
+    read and write different regions (8 of each, together well over the
+    256 MB Infinity Cache), so that, like the gather's rows, the data comes
+    from HBM and not from the cache. Each copy is timed between events recorded
+    around it alone (the markers add a little time; the kernel trace of
+    --copy-probe runs times the same copies exactly)."""
+    import torch
+    half = int(nbytes // 2)
+    a = torch.empty((regions, half), dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for i in range(3):
+        b[i % regions].copy_(a[(i + 3) % regions])
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for i, (e0, e1) in enumerate(ev):
+        e0.record()
+        b[i % regions].copy_(a[(i + 5) % regions])
+        e1.record()
+    torch.cuda.synchronize()
+    s = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev])) / 1e3
+    del a, b
+    return 2 * half / s / 1e9
+
+
 def alg_hbm_bytes(n, e, loc, hit, mis, rb):
     """HBM bytes one minibatch must move by the method's definition, whatever
     the implementation: per hop, the frontier row's id and CSR offsets (16 B),
@@ -247,6 +274,10 @@ def main():
         (sm["g_bytes"], sm["g_avg_s"] * 1e6, sm["g_gbps"], 100 * sm["g_gbps"] / HBM_PEAK_GBPS, sm["m_gbps"],
          sm["hit_rate"]))
 
+    copy_gbps = copy_reference(sm["g_bytes"])
+    log("plain device copy moving the same bytes (%d B): %.1f GB/s; the gather reaches %.1f%% of it" %
+        (round(sm["g_bytes"]), copy_gbps, 100 * sm["g_gbps"] / copy_gbps))
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, res["first_steps"])
@@ -277,7 +308,9 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "gather_hbm", "achieved": round(g_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(g_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": gather_traffic(sm["g_bytes"]) if w.name == "cl111m_p64" else None,
-                     "bytes_per_launch": round(sm["g_bytes"]), "avg_us": round(sm["g_avg_s"] * 1e6, 2)},
+                     "bytes_per_launch": round(sm["g_bytes"]), "avg_us": round(sm["g_avg_s"] * 1e6, 2),
+                     "plain_copy_same_bytes_GBps_events": round(copy_gbps, 1),
+                     "frac_of_plain_copy": round(sm["g_gbps"] / copy_gbps, 4)},
         "host_link": {"kernel": "gather_miss", "achieved": round(sm["m_gbps"], 2), "peak": PCIE_PEAK_GBPS,
                       "unit": "GB/s", "bytes_per_launch": round(sm["m_bytes"]),
                       "avg_us": round(sm["m_avg_us"], 2),

@@ -143,6 +143,14 @@ class Massive:
             lf = lf.contiguous()
         else:
             lf = np.ascontiguousarray(lf)
+        # the library copies L rows from local_feat and reads up to H rows of halo_store
+        nbytes = lambda x: x.numel() * x.element_size() if hasattr(x, "numel") else x.nbytes  # noqa: E731
+        if L > 0 and nbytes(lf) < int(L) * int(row_bytes):
+            raise ValueError("local_feat holds %d bytes, fewer than L * row_bytes" % nbytes(lf))
+        if H > 0 and nbytes(halo_store) < int(H) * int(row_bytes):
+            raise ValueError("halo_store holds %d bytes, fewer than H * row_bytes" % nbytes(halo_store))
+        if len(ip) != int(L) + int(H) + 1 or len(ix) < int(ip[-1]) or len(hg) < int(H) or len(hd) < int(H):
+            raise ValueError("indptr needs L + H + 1 entries, indices indptr[-1], halo_gid and halo_degree H each")
         if stream is None:
             stream = torch.cuda.current_stream()
         self.stream = stream
