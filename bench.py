@@ -150,19 +150,22 @@ def copy_reference(nbytes, reps=20, regions=8):
     --copy-probe runs times the same copies exactly)."""
     import torch
     half = int(nbytes // 2)
-    a = torch.empty((regions, half), dtype=torch.uint8, device="cuda").fill_(1)
+    stride = (half + 4095) // 4096 * 4096  # every region starts 4 KiB-aligned, as an allocation would
+    a = torch.empty(regions * stride, dtype=torch.uint8, device="cuda").fill_(1)
     b = torch.empty_like(a)
+    ra = [a[r * stride:r * stride + half] for r in range(regions)]
+    rb = [b[r * stride:r * stride + half] for r in range(regions)]
     for i in range(3):
-        b[i % regions].copy_(a[(i + 3) % regions])
+        rb[i % regions].copy_(ra[(i + 3) % regions])
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
     torch.cuda.synchronize()
     for i, (e0, e1) in enumerate(ev):
         e0.record()
-        b[i % regions].copy_(a[(i + 5) % regions])
+        rb[i % regions].copy_(ra[(i + 5) % regions])
         e1.record()
     torch.cuda.synchronize()
     s = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev])) / 1e3
-    del a, b
+    del a, b, ra, rb
     return 2 * half / s / 1e9
 
 
