@@ -67,7 +67,8 @@ struct massive_ctx {
   // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
   hipEvent_t ev_hbm_done[2] = {}, ev_batch_done[2] = {};
   hipEvent_t ev_miss_done[2] = {};  // the miss gather kernel alone (before its publish and mailbox copies)
-  hipEvent_t ev_swap_done = nullptr, ev_refill_done = nullptr;
+  hipEvent_t ev_round_done = nullptr, ev_refill_done = nullptr;
+  bool round_unclassified = false;  // a round was enqueued that no classify has waited for yet
   // The refill of the last round is copied in chunks, one after each of the
   // next steps' HBM gathers (host-link reads never overlap an HBM gather).
   int32_t round_id = 0;          // rounds so far, as stamped in slot_round / landed
@@ -100,6 +101,7 @@ struct massive_ctx {
   int32_t* d_landed = nullptr;        // [cap] round whose refill row has landed
   int32_t* d_part = nullptr;
   int32_t* d_part2 = nullptr;
+  int32_t* d_spart = nullptr;        // the sampler's scan partials (rounds use d_part, d_part2)
   int2* d_hbm_list = nullptr;
   int2* d_miss_list[2] = {};          // by step parity (read by the side stream)
   int32_t* d_miss_slot[2] = {};       // per miss-list entry: write-through slot or -1
@@ -363,7 +365,7 @@ void free_ctx(massive_ctx* c) {
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
-                 c->d_part, c->d_part2, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_miss_slot[0],
+                 c->d_part, c->d_part2, c->d_spart, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_miss_slot[0],
                  c->d_miss_slot[1], c->d_dummy, c->d_E, c->d_R,
                  c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
@@ -375,7 +377,7 @@ void free_ctx(massive_ctx* c) {
   if (c->h_ctr) (void)hipHostFree(c->h_ctr);
   for (hipEvent_t e : {c->ev_hbm_done[0], c->ev_hbm_done[1], c->ev_batch_done[0], c->ev_batch_done[1],
                        c->ev_miss_done[0], c->ev_miss_done[1],
-                       c->ev_swap_done, c->ev_refill_done})
+                       c->ev_round_done, c->ev_refill_done})
     if (e) (void)hipEventDestroy(e);
   for (auto& r : c->pending) {
     (void)hipEventDestroy(r.a);
@@ -436,7 +438,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
   for (hipEvent_t* e : {&c->ev_hbm_done[0], &c->ev_hbm_done[1], &c->ev_batch_done[0], &c->ev_batch_done[1],
                         &c->ev_miss_done[0], &c->ev_miss_done[1],
-                        &c->ev_swap_done, &c->ev_refill_done})
+                        &c->ev_round_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
 
   // the pinned store must be mapped into the device address space
@@ -471,6 +473,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_landed, cap * 4);
   CKA(c->d_part, c->pmax * 4);
   CKA(c->d_part2, c->pmax * 4);
+  CKA(c->d_spart, c->pmax * 4);
   CKA(c->d_hbm_list, R * 8);
   CKA(c->d_miss_list[0], R * 8);
   CKA(c->d_miss_list[1], R * 8);
@@ -655,8 +658,8 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       const int64_t nprev = nb[k - 1];
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
       ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, sz, k, c->fo[k - 1],
-                                                              io->indptr[k - 1], c->d_part, c->d_big, c->big_min);
-      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(sz, k, io->indptr[k - 1], c->d_part);
+                                                              io->indptr[k - 1], c->d_spart, c->d_big, c->big_min);
+      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(sz, k, io->indptr[k - 1], c->d_spart);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;
@@ -679,8 +682,8 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
                      s>>>(sa);
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_part);
-      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_part, io->nodes,
+      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart);
+      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart, io->nodes,
                                                              c->d_pos_of);
       ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], sz, k, c->d_pos_of);
     }
@@ -697,6 +700,12 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       (void)hipGetLastError();
       pend = c->round_id;
     }
+  }
+  // the round owed by the previous step ran on the copy stream beside this
+  // step's sampling; classify reads the buffer it rebuilt
+  if (c->round_unclassified) {
+    CK(hipStreamWaitEvent(s, c->ev_round_done, 0));
+    c->round_unclassified = false;
   }
   {
     massive_ctx::Range tr(c, s, 1);
@@ -817,18 +826,20 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   for (const void* p : {(const void*)evicted, (const void*)slots, (const void*)replaced})
     if (p && !device_visible(p)) return c->fail(MASSIVE_EINVAL, "an eviction output is not HIP-visible memory");
   c->pending_round = false;
-  hipStream_t s = c->s_main;
+  // The round runs on the copy stream, beside the next step's sampling on
+  // the main stream (the next classify waits for it). It follows, in stream
+  // order, the previous round's refill chunks, which read the fill list, the
+  // round state and the slot stamps that it rewrites; it starts after this
+  // step's classify and HBM gather (hit counts, scores; the gather runs alone).
+  hipStream_t s = c->s_copy;
   const int64_t cap = c->cap, H = c->H;
   ms::RoundState* rs = c->d_rs;
-  // the previous round's refill reads the fill list, the round state and the
-  // slot stamps that this round rewrites: finish it first
   {
     int rc = launch_refill_chunks(c, c->chunks_left, nullptr);
     if (rc != MASSIVE_OK) return rc;
   }
-  if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
-  c->refill_inflight = false;
   c->round_pending_rows = false;
+  CK(hipStreamWaitEvent(s, c->ev_hbm_done[tl & 1], 0));
   {
     massive_ctx::Range tr(c, s, 4);
     ms::k_materialize<<<grid_for(cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, cap, (int32_t)(c->t - c->mat_t),
@@ -871,19 +882,21 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
   }
-  // the refill is copied in chunks after the next steps' HBM gathers
-  CK(hipEventRecord(c->ev_swap_done, s));
-  CK(hipStreamWaitEvent(c->s_copy, c->ev_swap_done, 0));
-  // the last step's miss gather may still write rows of the previous round's
-  // replacements into slots this round reassigns: the new refill comes after it
-  CK(hipStreamWaitEvent(c->s_copy, c->ev_batch_done[tl & 1], 0));
+  if (k_out) {
+    CK(hipMemcpyAsync(&c->h_rs->k, &rs->k, 8, hipMemcpyDeviceToHost, s));
+    CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
+  }
+  CK(hipEventRecord(c->ev_round_done, s));
+  c->round_unclassified = true;
+  // the refill is copied in chunks after the next steps' HBM gathers; the last
+  // step's miss gather may still write rows of the previous round's
+  // replacements into slots this round reassigns, so the new refill comes after it
+  CK(hipStreamWaitEvent(s, c->ev_batch_done[tl & 1], 0));
   c->chunks_left = c->refill_chunks;
   c->round_pending_rows = true;
   CK(hipGetLastError());
   if (k_out) {
-    CK(hipMemcpyAsync(&c->h_rs->k, &rs->k, 8, hipMemcpyDeviceToHost, s));
-    CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
-    CK(hipStreamSynchronize(s));
+    CK(hipEventSynchronize(c->ev_round_done));
     if (c->h_ctr->bad) {
       c->broken = true;
       return c->fail(MASSIVE_EHIP, "eviction round produced inconsistent indices");
@@ -908,6 +921,7 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
   if (!c) return MASSIVE_EINVAL;
   hipStream_t s = c->s_main;
   CK(hipStreamSynchronize(c->s_miss));
+  if (c->round_unclassified) CK(hipStreamWaitEvent(s, c->ev_round_done, 0));
   if (c->cap > 0 && c->t > c->mat_t) {
     ms::k_materialize<<<grid_for(c->cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, c->cap,
                                                              (int32_t)(c->t - c->mat_t), c->gamma);
