@@ -144,13 +144,17 @@ int massive_batch_wait(massive_ctx* ctx, massive_batch* io);
 
 /* The eviction round owed by the step just sampled; must be called once after
  * every massive_sample / massive_sample_async. Runs the round iff that step t
- * has t > 0 and t mod delta == 0. The round is decided on the device: with
- * k_out == NULL the call only enqueues it; otherwise it waits and writes k'
- * (0 when no round is due). Optional device outputs, each with room for cap
- * entries: evicted halo ids, the slots they held (ascending), and their
- * replacements (entries [0, k')). The replacement rows are copied from
- * halo_store on a copy stream; until they have landed, the next steps read
- * hits on those slots from halo_store (the same bytes). */
+ * has t > 0 and t mod delta == 0. The round is decided on the device, on the
+ * library's copy stream, beside the next step's sampling (that step's lookup
+ * waits for it): with k_out == NULL the call only enqueues it; otherwise it
+ * waits for the round and writes k' (0 when no round is due). Optional device
+ * outputs, each with room for cap entries: evicted halo ids, the slots they
+ * held (ascending), and their replacements (entries [0, k')); they are
+ * complete when the call returns with k_out, or once the next step's
+ * massive_batch_wait has returned. The replacement rows are copied from
+ * halo_store on the copy stream; until they have landed, the next steps read
+ * hits on those slots from halo_store (the same bytes) and write them into
+ * their slots, so that no row crosses the host link twice. */
 int massive_evict_step(massive_ctx* ctx, int32_t* evicted, int32_t* slots, int32_t* replaced,
                        int64_t* k_out);
 
