@@ -61,7 +61,8 @@ struct massive_ctx {
   int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
   int32_t* d_big = nullptr;             // big-row list of the current hop
-  int64_t big_min = ms::kBigRow;        // rows longer than this use the 16-wave kernel
+  int64_t big_min = ms::kBigRow;        // rows longer than this are sampled by a whole block
+  int64_t big_blocks = ms::kBigBlocks;  // blocks that walk the list of such rows
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
   // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
@@ -433,6 +434,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   c->refill_chunks = std::max<int32_t>(1, std::min<int32_t>(a->delta - 1, 32));
   if (const char* e = getenv("MASSIVE_REFILL_CHUNKS")) c->refill_chunks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
+  if (const char* e = getenv("MASSIVE_BIG_BLOCKS")) c->big_blocks = std::max<int64_t>(1, atoll(e));
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
@@ -676,11 +678,21 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       sa.mu32 = c->mu32[k - 1];
       sa.big_min = c->big_min;
       sa.big_rows = c->d_big;
-      sa.row_waves = nprev;  // the big list never exceeds the frontier
       sa.pos_of = c->d_pos_of;
       sa.bits = c->d_bits;
-      ms::k_sample<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)), ms::kSampleWaves * MS_WAVE, 0,
-                     s>>>(sa);
+      // a small frontier is bound by its longest rows: a block each; a large
+      // one keeps the chip busy: a wave each, longest first
+      if (nprev <= ms::kBlockRowsMax) {
+        sa.row_waves = 0;
+        sa.big_blocks = std::max<int64_t>(1, std::min<int64_t>(nprev, c->big_blocks));
+        ms::k_sample_blocks<<<(unsigned)(sa.big_blocks + std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves))),
+                              ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
+      } else {
+        sa.row_waves = nprev;  // the big list never exceeds the frontier
+        sa.big_blocks = 0;
+        ms::k_sample_waves<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)),
+                             ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
+      }
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
       ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart);
       ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart, io->nodes,

@@ -156,13 +156,21 @@ __global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, in
 //      order (= ascending j), and the chosen positions are written in
 //      ascending j.
 // The chosen ids not yet in the frontier are marked in the new-node bitmap
-// as they are written. Rows longer than big_min (listed by k_row_counts) get
-// the first waves of the grid, so that the longest rows start first.
+// as they are written. Rows longer than big_min (listed by k_row_counts) are
+// taken first. Where the frontier is small, so that its few longest rows bound
+// the hop's time, each of them gets a whole block: its waves filter
+// consecutive quarters of the row with the same tau, and the four candidate
+// lists, concatenated in order, are the row's list in ascending j. Otherwise
+// (many rows keep the chip busy) each gets one wave, ahead of the shorter
+// rows. Other rows get one wave each.
 constexpr int kSampleWaves = 4;
 constexpr int kCandSlots = 5;                   // candidates per lane in the selection
 constexpr int kCandCap = kCandSlots * MS_WAVE;  // candidates per wave (LDS): 320, so the
                                                 // largest fanout (256) keeps 64 of slack for ties
 constexpr int64_t kBigRow = 2048;
+constexpr int64_t kBigBlocks = 2048;  // blocks that walk the big list (8 per CU)
+constexpr int64_t kBlockRowsMax = 65536;  // frontiers up to this size sample long rows by blocks
+constexpr int kTauIters = 64;         // threshold passes: x4 growth (<= 16) then bisection (<= 33)
 
 struct SampleArgs {
   const int64_t* csr_indptr;
@@ -178,7 +186,9 @@ struct SampleArgs {
   double mu32;              // (fo + 3 sqrt(fo) + 3) * 2^32
   int64_t big_min;          // rows longer than this are listed in big_rows
   const int32_t* big_rows;  // appended by k_row_counts
-  int64_t row_waves;        // waves [0, row_waves) walk the big list, the rest walk all rows
+  int64_t row_waves;        // k_sample_waves: waves [0, row_waves) take the big list, the rest all rows
+  int64_t big_blocks;       // k_sample_blocks: blocks [0, big_blocks) walk the big list, one row per
+                            // block; the rest take all other rows, one per wave
   const int32_t* pos_of;    // frontier position of an id, or -1
   uint32_t* bits;           // new-node bitmap
   int32_t* err;             // threshold search could not isolate a candidate set
@@ -278,7 +288,11 @@ __device__ __forceinline__ void select_emit(const uint64_t* list, int cnt, int f
   for (int b = top; b >= 0; --b) {
     const uint32_t trial = T | (1u << b);
     int c = __popcll(ballot(valid[0] && key[0] < trial));
-    for (int s = 1; s < S; ++s) c += __popcll(ballot(valid[s] && key[s] < trial));
+    // unrolled with static indices (a loop to S would index the arrays
+    // dynamically); S is the same in every lane
+#pragma unroll
+    for (int s = 1; s < kCandSlots; ++s)
+      if (s < S) c += __popcll(ballot(valid[s] && key[s] < trial));
     if (c < fo) T = trial;
   }
   int n_lt = 0;
@@ -309,7 +323,50 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) {
+// Filters 4-position groups [g0, g1) of a row of d positions: appends to c, in
+// ascending j, the candidates (key << 32 | j) whose key is <= tm1 (below tau),
+// stopping at kCandCap entries but counting them all. One wavefront.
+__device__ __forceinline__ int filter_groups(const PhiloxRow& ph, uint32_t g0, uint32_t g1, uint32_t d32,
+                                             uint32_t tm1, uint64_t* c) {
+  const int lane = lane_id();
+  int cnt = 0;
+  for (uint32_t q0 = g0; q0 < g1; q0 += MS_WAVE) {
+    const uint32_t q = q0 + lane;
+    const uint4 wv = ph(q);
+    // lane masks of the keys below tau, position j = 4q + s (held as scalar
+    // masks: the usual iteration of a long row takes none)
+    uint64_t m0, m1, m2, m3;
+    if (q0 + MS_WAVE <= g1 && 4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
+      m0 = ballot(wv.x <= tm1);
+      m1 = ballot(wv.y <= tm1);
+      m2 = ballot(wv.z <= tm1);
+      m3 = ballot(wv.w <= tm1);
+    } else {
+      const bool in = q < g1;
+      m0 = ballot(in && 4 * q < d32 && wv.x <= tm1);
+      m1 = ballot(in && 4 * q + 1 < d32 && wv.y <= tm1);
+      m2 = ballot(in && 4 * q + 2 < d32 && wv.z <= tm1);
+      m3 = ballot(in && 4 * q + 3 < d32 && wv.w <= tm1);
+    }
+    if (!(m0 | m1 | m2 | m3)) continue;
+    // candidates in ascending j: lower lanes first, then s within the lane
+    int p = cnt + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+    const uint64_t bit = 1ull << lane;
+    const uint64_t m[4] = {m0, m1, m2, m3};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      if (m[s] & bit) {
+        if (p < kCandCap) c[p] = ((uint64_t)word_of(wv, s) << 32) | (4 * q + s);
+        ++p;
+      }
+    cnt += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+  }
+  return cnt;
+}
+
+// Large frontiers (many rows keep the chip busy): every row one per wave, the
+// long ones (waves [0, row_waves) walk the big list) dispatched first.
+__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_waves(SampleArgs a) {
   __shared__ uint64_t cand[kSampleWaves][kCandCap];
   if (a.sz->status) return;
   const int lane = lane_id(), wave = wave_uniform(wave_id());
@@ -338,10 +395,10 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) 
   TauSearch ts;
   ts.tau = first_tau(a.mu32, d);
   int cnt = 0;
-  bool fail = false;
+  bool fail = false, ok = false;
   const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
   const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
-  for (int iter = 0; iter < 48 && !fail; ++iter) {
+  for (int iter = 0; iter < kTauIters && !fail; ++iter) {
     cnt = 0;
     const uint32_t tm1 = (uint32_t)(ts.tau - 1);  // key < tau  <=>  key <= tau - 1
     for (uint32_t q0 = 0; 4 * q0 < d32; q0 += MS_WAVE) {
@@ -374,14 +431,113 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample(SampleArgs a) 
         }
       cnt += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
     }
-    if (ts.step(cnt, fo, kCandCap, &fail)) break;
+    if (ts.step(cnt, fo, kCandCap, &fail)) {
+      ok = true;
+      break;
+    }
   }
-  if (fail) {
+  if (!ok) {
     if (lane == 0) atomicOr(a.err, 4);
     return;
   }
   wave_lds_sync();
   select_emit(c, cnt, fo, ts.tau, nb, out, a.pos_of, a.bits);
+}
+
+// One row by one wavefront (skipped if it is longer than skip_above).
+__device__ __forceinline__ void sample_row_wave(const SampleArgs& a, int64_t row, uint64_t* c,
+                                                int64_t skip_above = INT64_MAX) {
+  const int lane = lane_id();
+  const int32_t fo = a.fo;
+  // the row, its node and its extent are the same in every lane
+  const int32_t v = wave_uniform(a.nodes[row]);
+  const int64_t start = wave_uniform(a.csr_indptr[v]);
+  const int64_t d = wave_uniform(a.csr_indptr[v + 1]) - start;
+  if (d > skip_above) return;
+  int32_t* out = a.out + a.bptr[row];
+  const int32_t* nb = a.csr_indices + start;
+  if (d <= fo) {
+    for (int64_t j = lane; j < d; j += MS_WAVE) emit_id(out, (int)j, nb[j], a.pos_of, a.bits);
+    return;
+  }
+  TauSearch ts;
+  ts.tau = first_tau(a.mu32, d);
+  int cnt = 0;
+  bool fail = false, ok = false;
+  const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
+  const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
+  for (int iter = 0; iter < kTauIters && !ok && !fail; ++iter) {
+    cnt = filter_groups(ph, 0, (d32 + 3) / 4, d32, (uint32_t)(ts.tau - 1), c);
+    ok = ts.step(cnt, fo, kCandCap, &fail);
+  }
+  if (!ok) {
+    if (lane == 0) atomicOr(a.err, 4);
+    return;
+  }
+  wave_lds_sync();
+  select_emit(c, cnt, fo, ts.tau, nb, out, a.pos_of, a.bits);
+  // (a wave samples one row: no fence at the end, which would hold the wave
+  // until its stores and bitmap atomics have completed)
+}
+
+// Small frontiers: the long rows one per block, the blocks walking the big
+// list; every other row one per wave.
+__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_blocks(SampleArgs a) {
+  __shared__ uint64_t cand[kSampleWaves][kCandCap];
+  if (a.sz->status) return;
+  const int lane = lane_id(), wave = wave_uniform(wave_id());
+  const int32_t fo = a.fo;
+  if ((int64_t)blockIdx.x < a.big_blocks) {
+    __shared__ uint64_t merged[kCandCap];
+    __shared__ int counts[kSampleWaves];
+    // long rows, one per block at a time
+    const int64_t n_big = a.sz->n_big[a.hop - 1];
+    for (int64_t b = blockIdx.x; b < n_big; b += a.big_blocks) {
+      const int64_t row = wave_uniform((int32_t)a.big_rows[b]);
+      const int32_t v = wave_uniform(a.nodes[row]);
+      const int64_t start = wave_uniform(a.csr_indptr[v]);
+      const int64_t d = wave_uniform(a.csr_indptr[v + 1]) - start;  // > big_min >= fo
+      int32_t* out = a.out + a.bptr[row];
+      const int32_t* nb = a.csr_indices + start;
+      const uint32_t d32 = (uint32_t)d;
+      const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
+      // this wave's quarter of the row's groups, in whole wave iterations
+      const uint32_t groups = (d32 + 3) / 4;
+      const uint32_t per = (groups + kSampleWaves * MS_WAVE - 1) / (kSampleWaves * MS_WAVE) * MS_WAVE;
+      const uint32_t g0 = min(groups, (uint32_t)wave * per), g1 = min(groups, g0 + per);
+      TauSearch ts;
+      ts.tau = first_tau(a.mu32, d);
+      int total = 0;
+      bool fail = false, ok = false;
+      for (int iter = 0; iter < kTauIters; ++iter) {
+        const int cnt = filter_groups(ph, g0, g1, d32, (uint32_t)(ts.tau - 1), cand[wave]);
+        if (lane == 0) counts[wave] = cnt;
+        __syncthreads();
+        total = 0;
+        for (int x = 0; x < kSampleWaves; ++x) total += counts[x];
+        // every wave takes the same decision from the same total
+        ok = ts.step(total, fo, kCandCap, &fail);
+        if (ok || fail) break;
+        __syncthreads();  // the next pass rewrites cand and counts
+      }
+      if (!ok) {
+        if (threadIdx.x == 0) atomicOr(a.err, 4);
+        return;  // every wave of the block leaves together
+      }
+      // the four lists, in order, are the row's candidates in ascending j
+      int before = 0;
+      for (int x = 0; x < wave; ++x) before += counts[x];
+      for (int i = lane; i < counts[wave]; i += MS_WAVE) merged[before + i] = cand[wave][i];
+      __syncthreads();
+      if (wave == 0) select_emit(merged, total, fo, ts.tau, nb, out, a.pos_of, a.bits);
+      if (b + a.big_blocks < n_big) __syncthreads();  // merged and counts are reused for the next row
+    }
+    return;
+  }
+  const int64_t row = (int64_t)(blockIdx.x - a.big_blocks) * kSampleWaves + wave;
+  if (row >= a.sz->n[a.hop - 1]) return;
+  // rows longer than big_min are taken by the big list
+  sample_row_wave(a, row, cand[wave], a.big_min);
 }
 
 // ------------------------------------------------------------ dedup/relabel

@@ -119,3 +119,19 @@ def test_row_offsets_past_2_31():
         assert np.array_equal(feat, src)
         gm.evict_step()
     log("offsets: done (%.0fs)" % (time.time() - t0))
+
+
+@pytest.mark.parametrize("big_row,big_blocks", [(256, 3), (300, 2048)])
+def test_long_rows_by_blocks(monkeypatch, big_row, big_blocks):
+    # rows longer than big_row are sampled by a whole block (four waves over
+    # consecutive quarters of the row); few blocks make each walk many rows
+    monkeypatch.setenv("MASSIVE_BIG_ROW", str(big_row))
+    monkeypatch.setenv("MASSIVE_BIG_BLOCKS", str(big_blocks))
+    prob, sched, w = workload_problem("cl170k", delta=2)
+    deg = np.diff(prob.indptr)
+    assert np.sum(deg > big_row) > 100
+    rounds, _, _ = run_parity("cl170k big rows > %d, %d blocks" % (big_row, big_blocks), prob, sched.seeds, 5,
+                              state_every=2)
+    assert rounds == 2
+    prob, sched, w = workload_problem("cl10k", fanout=(200, 30), delta=3)
+    run_parity("cl10k fanout 200 big rows > %d" % big_row, prob, sched.seeds, 6)
