@@ -9,6 +9,10 @@ namespace ms {
 
 constexpr uint64_t kEmpty = ~0ull;
 
+// 16- and 8-byte vectors of the copy kernels and the table windows
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+
 // MurmurHash3 fmix32 finaliser (public domain).
 __device__ __forceinline__ uint32_t fmix32(uint32_t x) {
   x ^= x >> 16;
@@ -22,6 +26,18 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t x) {
 // Open-addressing table (linear probing, load <= 1/2): entry = slot << 32 | h.
 __device__ __forceinline__ int32_t hash_find(const uint64_t* __restrict__ tab, uint32_t mask, int32_t h) {
   uint32_t i = fmix32((uint32_t)h) & mask;
+  while (true) {
+    const uint64_t e = tab[i];
+    if ((uint32_t)e == (uint32_t)h) return (int32_t)(e >> 32);
+    if (e == kEmpty) return -1;
+    i = (i + 1) & mask;
+  }
+}
+
+// The same search continued from entry i (after a window of entries that
+// held neither h nor an empty entry).
+__device__ __forceinline__ int32_t hash_find_from(const uint64_t* __restrict__ tab, uint32_t mask, int32_t h,
+                                                  uint32_t i) {
   while (true) {
     const uint64_t e = tab[i];
     if ((uint32_t)e == (uint32_t)h) return (int32_t)(e >> 32);
@@ -80,6 +96,12 @@ constexpr int kClsItems = 8;  // rows per thread: one block classifies 2048 rows
 
 // Block-level aggregation: each block counts its rows per class, takes one
 // base per list with a single atomic, and places rows with wave ballots.
+// The loads of a thread go out in three rounds, each for all its rows: the
+// frontier ids; a window of four table entries from each id's probe start
+// (the 16-byte pairs holding entries p & ~1 .. (p & ~1) + 3, which settle
+// almost every search; the rare rest probes on one by one); the hit slots'
+// counters and refill stamps. Lanes past the end and local rows load dummy
+// (in-range) addresses and change nothing.
 __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   constexpr int NW = kClsNT / MS_WAVE;
   __shared__ int32_t wc[NW][4];          // per-wave counts: hbm list, host list, local, pending hits
@@ -88,43 +110,96 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   const int64_t n = a.sz->n[a.K];
   const int lane = lane_id(), wave = wave_id();
   const int64_t tile = (int64_t)kClsNT * kClsItems;
+  const bool pending = a.pend_round >= 0;
   for (int64_t b0 = (int64_t)blockIdx.x * tile; b0 < n; b0 += (int64_t)gridDim.x * tile) {
+    int32_t v[kClsItems], slot[kClsItems];
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) {
+      // wave w of item it covers rows b0 + it*256 + w*64 + lane
+      const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
+      v[it] = a.nodes[i < n ? i : n - 1];
+    }
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) pin(v[it]);
+    {
+      v4u w0[kClsItems], w1[kClsItems];
+#pragma unroll
+      for (int it = 0; it < kClsItems; ++it) {
+        const uint32_t q = (fmix32((uint32_t)(v[it] - a.L)) & a.tmask) & ~1u;
+        w0[it] = *reinterpret_cast<const v4u*>(a.tab + q);
+        w1[it] = *reinterpret_cast<const v4u*>(a.tab + ((q + 2) & a.tmask));
+      }
+#pragma unroll
+      for (int it = 0; it < kClsItems; ++it) {
+        pin(w0[it]);
+        pin(w1[it]);
+      }
+#pragma unroll
+      for (int it = 0; it < kClsItems; ++it) {
+        const int32_t h = v[it] - a.L;
+        const uint32_t p = fmix32((uint32_t)h) & a.tmask;
+        const uint64_t e[4] = {((uint64_t)w0[it].y << 32) | w0[it].x, ((uint64_t)w0[it].w << 32) | w0[it].z,
+                               ((uint64_t)w1[it].y << 32) | w1[it].x, ((uint64_t)w1[it].w << 32) | w1[it].z};
+        int32_t r = -2;  // -2: not settled by the window
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+          if (r == -2 && x >= (int)(p & 1u)) {
+            if ((uint32_t)e[x] == (uint32_t)h) r = (int32_t)(e[x] >> 32);
+            else if (e[x] == kEmpty) r = -1;
+          }
+        if (v[it] < a.L) r = -1;
+        else if (r == -2) r = hash_find_from(a.tab, a.tmask, h, ((p & ~1u) + 4) & a.tmask);
+        slot[it] = r;
+      }
+    }
+    int32_t hc[kClsItems], sr[kClsItems], ld[kClsItems];
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) {
+      const int32_t sl = slot[it] >= 0 ? slot[it] : 0;
+      hc[it] = a.hitcnt[sl];
+      sr[it] = 0;
+      ld[it] = 0;
+      if (pending) {  // the same in every lane
+        sr[it] = a.slot_round[sl];
+        ld[it] = __hip_atomic_load(&a.landed[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < kClsItems; ++it) {
+      pin(hc[it]);
+      pin(sr[it]);
+      pin(ld[it]);
+    }
     int cls[kClsItems];
     int32_t src[kClsItems], wslot[kClsItems];
     int ch = 0, cm = 0, cl = 0, cp = 0;  // hbm list, host list, local, pending hits
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
-      // wave w of item it covers rows b0 + it*256 + w*64 + lane
       const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
       cls[it] = -1;
       src[it] = 0;
       wslot[it] = -1;
       if (i < n) {
-        const int32_t v = a.nodes[i];
-        a.pos_of[v] = -1;
-        if (v < a.L) {
+        a.pos_of[v[it]] = -1;
+        const int32_t h = v[it] - a.L;
+        if (v[it] < a.L) {
           cls[it] = 0;
-          src[it] = v;
-        } else {
-          const int32_t h = v - a.L;
-          const int32_t slot = hash_find(a.tab, a.tmask, h);
-          if (slot >= 0) {
-            cls[it] = 1;
-            src[it] = a.L + slot;
-            a.hitcnt[slot] += 1;
-            // a hit on a slot whose refill may not have landed reads the same
-            // row from the host store
-            if (a.pend_round >= 0 && a.slot_round[slot] == a.pend_round &&
-                __hip_atomic_load(&a.landed[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.pend_round) {
-              cls[it] = 3;
-              src[it] = h;
-              wslot[it] = slot;
-            }
-          } else {
-            cls[it] = 2;
+          src[it] = v[it];
+        } else if (slot[it] >= 0) {
+          cls[it] = 1;
+          src[it] = a.L + slot[it];
+          a.hitcnt[slot[it]] = hc[it] + 1;
+          // a hit on a slot whose refill may not have landed reads the same
+          // row from the host store
+          if (pending && sr[it] == a.pend_round && ld[it] != a.pend_round) {
+            cls[it] = 3;
             src[it] = h;
-            atomicAdd(&a.S_A[h], 1.0f);
+            wslot[it] = slot[it];
           }
+        } else {
+          cls[it] = 2;
+          src[it] = h;
+          atomicAdd(&a.S_A[h], 1.0f);
         }
         a.mask[i] = (uint8_t)(cls[it] == 3 ? 1 : cls[it]);
       }
@@ -188,8 +263,6 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
 // past the end re-reads its first chunk, or, where re-reading costs host-link
 // bytes, a dummy device row; the loaded values are pinned with an empty asm
 // before the predicated stores.
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
 // chunk cc of the flattened space -> (list entry, byte offset in the row);
 // ONE: one chunk per row (no division)

@@ -40,6 +40,15 @@ __device__ __forceinline__ T wave_inclusive_scan(T x) {
   return x;
 }
 
+// Keeps a loaded value where it is: an empty asm that reads and writes it.
+// Loads whose values are only used under a per-lane condition are otherwise
+// sunk by the compiler into that condition, each behind its own wait, so the
+// loads of a thread would be issued one at a time.
+template <typename T>
+__device__ __forceinline__ void pin(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T x) {
 #pragma unroll

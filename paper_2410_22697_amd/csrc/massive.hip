@@ -659,8 +659,11 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     for (int k = 1; k <= c->K; ++k) {
       const int64_t nprev = nb[k - 1];
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
-      ms::k_row_counts<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(c->d_indptr, io->nodes, sz, k, c->fo[k - 1],
-                                                              io->indptr[k - 1], c->d_spart, c->d_big, c->big_min);
+      // the previous hop's relabel shares the launch
+      const int64_t nrel = k > 1 ? (int64_t)grid_for(eb[k - 2], ms::kScanTile, 1024) : 0;
+      ms::k_row_counts<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
+          c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], c->d_spart, c->d_big, c->big_min, nbk,
+          k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
       ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(sz, k, io->indptr[k - 1], c->d_spart);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
@@ -697,7 +700,9 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart);
       ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart, io->nodes,
                                                              c->d_pos_of);
-      ms::k_relabel<<<grid_for(eb[k - 1], 256), 256, 0, s>>>(io->indices[k - 1], sz, k, c->d_pos_of);
+      if (k == c->K)
+        ms::k_relabel<<<grid_for(eb[k - 1], ms::kScanTile, 1024), ms::kScanNT, 0, s>>>(io->indices[k - 1], sz, k,
+                                                                                     c->d_pos_of);
     }
   }
   // A refill that may still be in flight: hits on its slots read the host

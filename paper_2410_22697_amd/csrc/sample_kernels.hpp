@@ -51,39 +51,99 @@ __global__ void k_seed_undo(const int32_t* __restrict__ seeds, int32_t n0, int32
 }
 
 // ------------------------------------------------------ per-row counts + scan
-// Block b: sum over its tile of min(deg(F[i]), fo); counts go to out[i+1].
+// Block b < nbk: sum over its tile of min(deg(F[i]), fo); counts go to
+// bptr[i+1], rows longer than big_min to big_rows (one global atomic per
+// block). Every load of a thread is issued before the first is used.
+// Blocks b >= nbk relabel the previous hop's sampled ids (rel_ids, if given):
+// that work depends on the same kernels and shares the launch.
+__device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t e, const int32_t* __restrict__ pos_of,
+                                              int64_t b, int64_t nblocks) {
+  for (int64_t b0 = b * kScanTile; b0 < e; b0 += nblocks * kScanTile) {
+    int32_t u[kScanItems], p[kScanItems];
+    // lanes past the end read the last id (or its new value, also a valid
+    // index) and store nothing
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      const int64_t i = b0 + (int64_t)it * kScanNT + threadIdx.x;
+      u[it] = ids[i < e ? i : e - 1];
+    }
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) pin(u[it]);
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) p[it] = pos_of[u[it]];
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) pin(p[it]);
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      const int64_t i = b0 + (int64_t)it * kScanNT + threadIdx.x;
+      if (i < e) ids[i] = p[it];
+    }
+  }
+}
+
 __global__ __launch_bounds__(kScanNT) void k_row_counts(const int64_t* __restrict__ csr_indptr,
                                                         const int32_t* __restrict__ nodes,
                                                         StepSizes* sz, int hop, int32_t fo,
                                                         int32_t* __restrict__ bptr,
                                                         int32_t* __restrict__ partials,
-                                                        int32_t* __restrict__ big_rows, int64_t big_min) {
+                                                        int32_t* __restrict__ big_rows, int64_t big_min, int64_t nbk,
+                                                        int32_t* __restrict__ rel_ids,
+                                                        const int32_t* __restrict__ pos_of) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  __shared__ int32_t big_lds[kScanTile];
+  __shared__ int32_t big_n;
+  __shared__ unsigned long long big_base;
   if (sz->status) return;
+  if ((int64_t)blockIdx.x >= nbk) {
+    if (rel_ids) relabel_tiles(rel_ids, sz->e[hop - 2], pos_of, blockIdx.x - nbk, gridDim.x - nbk);
+    return;
+  }
   const int64_t n = sz->n[hop - 1];
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  if (threadIdx.x == 0) big_n = 0;
+  __syncthreads();
   int32_t s = 0;
+  if (base < n) {
+    int32_t v[kScanItems];
+    int64_t lo[kScanItems], hi[kScanItems];
 #pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
-    if (i < n) {
-      const int32_t v = nodes[i];
-      const int64_t d = csr_indptr[v + 1] - csr_indptr[v];
-      const int32_t c = d < fo ? (int32_t)d : fo;
-      bptr[i + 1] = c;
-      s += c;
-      if (d > big_min) {
-        const unsigned long long b = atomicAdd((unsigned long long*)&sz->n_big[hop - 1], 1ull);
-        big_rows[b] = (int32_t)i;
+    for (int it = 0; it < kScanItems; ++it) {
+      const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
+      v[it] = nodes[i < n ? i : n - 1];
+    }
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) pin(v[it]);
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      lo[it] = csr_indptr[v[it]];
+      hi[it] = csr_indptr[v[it] + 1];
+    }
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      pin(lo[it]);
+      pin(hi[it]);
+    }
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
+      if (i < n) {
+        const int64_t d = hi[it] - lo[it];
+        const int32_t c = d < fo ? (int32_t)d : fo;
+        bptr[i + 1] = c;
+        s += c;
+        if (d > big_min) big_lds[atomicAdd(&big_n, 1)] = (int32_t)i;
       }
     }
   }
-  s = block_sum<kScanNT>(s, lds);
+  s = block_sum<kScanNT>(s, lds);  // (its barriers also complete the big_lds appends)
   if (threadIdx.x == 0) {
     partials[blockIdx.x] = s;
     if (s) atomicAdd((unsigned long long*)&sz->e[hop - 1], (unsigned long long)s);
     if (blockIdx.x == 0) sz->n[hop] = n;  // new nodes are added by k_bits_count
+    big_base = big_n ? atomicAdd((unsigned long long*)&sz->n_big[hop - 1], (unsigned long long)big_n) : 0ull;
   }
+  __syncthreads();
+  for (int j = threadIdx.x; j < big_n; j += kScanNT) big_rows[big_base + j] = big_lds[j];
 }
 
 // Exclusive scan of partials[0..nb) in place (one block). Writes the total
@@ -600,14 +660,12 @@ __global__ __launch_bounds__(kScanNT) void k_bits_emit(uint32_t* __restrict__ bi
   }
 }
 
-// Relabel sampled ids to their frontier positions.
-__global__ void k_relabel(int32_t* __restrict__ ids, const StepSizes* sz, int hop,
-                          const int32_t* __restrict__ pos_of) {
+// Relabel the last hop's sampled ids to their frontier positions (earlier
+// hops are relabelled by the next hop's k_row_counts).
+__global__ __launch_bounds__(kScanNT) void k_relabel(int32_t* __restrict__ ids, const StepSizes* sz, int hop,
+                                                     const int32_t* __restrict__ pos_of) {
   if (sz->status) return;
-  const int64_t e = sz->e[hop - 1];
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < e;
-       i += (int64_t)gridDim.x * blockDim.x)
-    ids[i] = pos_of[ids[i]];
+  relabel_tiles(ids, sz->e[hop - 1], pos_of, blockIdx.x, gridDim.x);
 }
 
 }  // namespace ms
