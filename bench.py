@@ -24,6 +24,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
+# Batches in flight in the timed loop (the library allows up to three): with
+# two, the next step's sampling overlaps the current step's host-link reads
+# and never the HBM gather; a third lets sampling run beside the HBM gather
+# too, which slows it, with no gain while the host link bounds the step.
+DEFAULT_DEPTH = 2
 PCIE_PEAK_GBPS = 64.0        # PCIe 5.0 x16, one direction
 
 
@@ -65,11 +70,13 @@ def build_inputs(w, threads=None):
     return g, local, store, sched
 
 
-def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False):
-    """One context over steps 0..warmup+steps-1 with look-ahead; the last
-    `steps` are timed. Returns the raw measurements."""
+def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False, depth=None):
+    """One context over steps 0..warmup+steps-1 with look-ahead (`depth`
+    batches in flight); the last `steps` are timed. Returns the raw
+    measurements."""
     import torch
     from paper_2410_22697_amd import Massive
+    depth = depth or DEFAULT_DEPTH
     torch.cuda.set_device(0)
     t0 = time.time()
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
@@ -77,7 +84,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     torch.cuda.synchronize()
     init_s = time.time() - t0
     log("massive_init %.2fs: cap=%d alpha=%.6g" % (init_s, gm.cap, gm.alpha))
-    bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
+    bbs = [gm.alloc_batch(w.batch) for _ in range(depth)]
     total = warmup + steps
     seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
     torch.cuda.synchronize()
@@ -95,28 +102,32 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     stats = []        # per step: local, hits, misses, rows, host-link rows
     sizes = []        # per step: frontier sizes n_0..n_K and sampled edges e_1..e_K
 
+    def finish(u):
+        r = gm.wait(bbs[u % depth])
+        stats.append((r.local, r.hits, r.misses, r.n[-1], r.host_rows))
+        sizes.append((list(r.n), list(r.e)))
+        if u < 2 and len(first_steps) == u:
+            bb = bbs[u % depth]
+            nK = r.n[-1]
+            first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
+                                bb.feat[:nK].cpu().numpy().copy()))
+        if log_steps:
+            log("step %d local %d hits %d misses %d rows %d host %d" % (u, r.local, r.hits, r.misses, r.n[-1],
+                                                                        r.host_rows))
+
     def run(t0, t1):
-        """Steps t0..t1-1 with look-ahead: step t+1 is enqueued (after step t's
-        round) before step t is waited for, so its sampling overlaps step t's
-        host-link reads."""
-        prev = None
-        for t in range(t0, t1 + 1):
-            if t < t1:
-                gm.sample_async(seeds_dev[t], bbs[t % 2])
-                gm.evict_step(wait=False)
-            if prev is not None:
-                r = gm.wait(bbs[prev % 2])
-                stats.append((r.local, r.hits, r.misses, r.n[-1], r.host_rows))
-                sizes.append((list(r.n), list(r.e)))
-                if prev < 2 and len(first_steps) == prev:
-                    bb = bbs[prev % 2]
-                    nK = r.n[-1]
-                    first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
-                                        bb.feat[:nK].cpu().numpy().copy()))
-                if log_steps:
-                    log("step %d local %d hits %d misses %d rows %d host %d" % (prev, r.local, r.hits, r.misses,
-                                                                                r.n[-1], r.host_rows))
-            prev = t
+        """Steps t0..t1-1 with look-ahead: step t is enqueued (after step t-1's
+        round) before step t - depth + 1 is waited for, so the sampling of the
+        next steps overlaps the host-link reads of earlier ones."""
+        inflight = []
+        for t in range(t0, t1):
+            gm.sample_async(seeds_dev[t], bbs[t % depth])
+            gm.evict_step(wait=False)
+            inflight.append(t)
+            if len(inflight) == depth:
+                finish(inflight.pop(0))
+        for u in inflight:
+            finish(u)
 
     run(0, warmup)
     log("warmup %d steps done" % warmup)
@@ -132,6 +143,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     r1, e1 = gm.counters()
     f1 = gm.refilled_rows()
     out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
+               depth=depth,
                stats=np.array(stats, np.float64), sizes=sizes, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
                refilled=f1 - f0, first_steps=first_steps)
     del bbs, seeds_dev
@@ -223,6 +235,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--threads", type=int, default=None)
     ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
+    ap.add_argument("--depth", type=int, default=DEFAULT_DEPTH, help="batches in flight (1 to 3)")
     ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
     ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
     ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
@@ -262,7 +275,8 @@ def main():
         overlap(w, g, local, store, sched, args)
         return
 
-    res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe)
+    res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe,
+                      args.depth)
     sm = summarize(w, res)
     K, rb = args.steps, w.row_bytes
     log("timed %d steps in %.3fs: %.1f minibatches/s, %d rounds, %d evicted" %
@@ -303,7 +317,7 @@ def main():
                    "L": g.L, "H": g.H, "csr_entries": g.nnz, "batch": w.batch, "fanout": list(w.fanout),
                    "row_bytes": rb, "buffer_pct": w.buffer_pct, "gamma": w.gamma, "delta": w.delta,
                    "cap": res["gm_cap"], "steps_timed": [args.warmup, args.warmup + K - 1],
-                   "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"], "lookahead": 1,
+                   "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"], "lookahead": res["depth"] - 1,
                    "parallelism": "one partition on one GPU"},
         "gather_GBps": round(g_gbps, 1),
         "gather_frac_hbm": round(g_gbps / HBM_PEAK_GBPS, 4),

@@ -60,6 +60,7 @@ extern "C" {
 #define MASSIVE_ESTATE (-5)    /* call out of order (see massive_sample)      */
 
 #define MASSIVE_MAX_HOPS 8
+#define MASSIVE_MAX_INFLIGHT 3 /* batches enqueued and not yet waited for */
 
 typedef struct massive_ctx massive_ctx;
 
@@ -132,9 +133,10 @@ int massive_sample(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, mass
  * prepares the next minibatch while the current one is consumed): enqueues
  * the step and returns at once. The batch's buffers must not be read or
  * reused, and its sizes are not written, until massive_batch_wait returns for
- * it. At most two batches are in flight: the next step can be enqueued (after
- * its predecessor's massive_evict_step) while the previous one still reads
- * misses over the host link. Argument errors are returned here; seed errors
+ * it. At most MASSIVE_MAX_INFLIGHT batches are in flight: the next steps can
+ * be enqueued (each after its predecessor's massive_evict_step) while earlier
+ * ones still read misses over the host link; a further one is refused with
+ * MASSIVE_ESTATE. Argument errors are returned here; seed errors
  * are returned by massive_batch_wait (if a later step was already issued the
  * context then refuses further work with MASSIVE_ESTATE). */
 int massive_sample_async(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);

@@ -4,5 +4,5 @@
 `Massive` is the only entry point; every step runs in libmassive's HIP
 kernels. Importing `Massive` raises if libmassive.so has not been built.
 """
-from .massive import (EXPORTS, LIB_PATH, TIMING_GROUPS, BatchBuffers, Massive,  # noqa: F401
+from .massive import (EXPORTS, LIB_PATH, MAX_INFLIGHT, TIMING_GROUPS, BatchBuffers, Massive,  # noqa: F401
                       MassiveError, StepResult, load)

@@ -314,7 +314,7 @@ __global__ __launch_bounds__(256) void k_gather_hbm(const int2* __restrict__ lis
 // also holds the hits on slots whose refill had not landed when the step was
 // classified; such a row is written into its buffer slot too (wslot >= 0), so
 // a replacement row crosses the link once, together with the misses (the
-// merged fetch of Algorithm 2). k_publish then marks those slots landed.
+// merged fetch of Algorithm 2). k_step_done then marks those slots landed.
 // dummy: a device row of row_bytes that lanes past the end move onto itself.
 template <typename V, bool ONE>
 __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int32_t* __restrict__ wslot,
@@ -357,14 +357,29 @@ __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ li
   }
 }
 
-// After k_gather_miss (a kernel boundary: its row writes are complete): the
-// written-through slots are landed for round `round_id`.
-__global__ void k_publish(const int32_t* __restrict__ wslot, const int64_t* __restrict__ count,
-                          int32_t* __restrict__ landed, int64_t cap, int32_t round_id) {
-  const int64_t n = *count;
-  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t ws = wslot[x];
-    if (ws >= 0 && ws < cap) __hip_atomic_store(&landed[ws], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// The step's last kernel, after k_gather_miss (a kernel boundary: its row
+// writes are complete): the written-through slots are landed for round
+// `round_id` (none if round_id < 0), and block 0 copies the step's sizes and
+// the eviction-round consistency flag into the pinned host mailbox (device
+// view), made visible to the host before the kernel ends.
+constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
+static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
+__global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ wslot,
+                                                   const int64_t* __restrict__ count, int32_t* __restrict__ landed,
+                                                   int64_t cap, int32_t round_id, const StepSizes* __restrict__ sz,
+                                                   const int32_t* __restrict__ bad, StepSizes* h_sz, int32_t* h_bad) {
+  if (round_id >= 0) {
+    const int64_t n = *count;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x) {
+      const int32_t ws = wslot[x];
+      if (ws >= 0 && ws < cap) __hip_atomic_store(&landed[ws], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (blockIdx.x == 0) {
+    const int i = threadIdx.x;
+    if (i < kSizeWords) reinterpret_cast<int32_t*>(h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
+    if (i == kSizeWords) *h_bad = *bad;
+    __threadfence_system();
   }
 }
 

@@ -40,6 +40,8 @@ inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
 
 }  // namespace
 
+constexpr int kSlots = MASSIVE_MAX_INFLIGHT;
+
 struct massive_ctx {
   // configuration
   int32_t L = 0, H = 0;
@@ -65,9 +67,10 @@ struct massive_ctx {
   int64_t big_blocks = ms::kBigBlocks;  // blocks that walk the list of such rows
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
-  // per step parity: classify -> HBM gather done (main), miss gather + mailbox done (side)
-  hipEvent_t ev_hbm_done[2] = {}, ev_batch_done[2] = {};
-  hipEvent_t ev_miss_done[2] = {};  // the miss gather kernel alone (before its publish and mailbox copies)
+  // per step slot (step t uses slot t % MASSIVE_MAX_INFLIGHT): classify done
+  // (main), HBM gather done and miss gather + mailbox done (side)
+  hipEvent_t ev_cls_done[kSlots] = {}, ev_hbm_done[kSlots] = {}, ev_batch_done[kSlots] = {};
+  hipEvent_t ev_miss_done[kSlots] = {};  // the miss gather kernel (its write-through rows are in place)
   hipEvent_t ev_round_done = nullptr, ev_refill_done = nullptr;
   bool round_unclassified = false;  // a round was enqueued that no classify has waited for yet
   // The refill of the last round is copied in chunks, one after each of the
@@ -91,9 +94,11 @@ struct massive_ctx {
   uint64_t* d_tab = nullptr;
   int32_t* d_pos_of = nullptr;
   uint32_t* d_bits = nullptr;
-  ms::StepSizes* d_sz = nullptr;      // [2], by step parity
-  ms::StepSizes* h_sz = nullptr;      // [2] pinned mailboxes
-  int32_t* h_bad = nullptr;           // [2] pinned: eviction-round consistency flag
+  ms::StepSizes* d_sz = nullptr;      // [kSlots], by step slot
+  ms::StepSizes* h_sz = nullptr;      // [kSlots] pinned mailboxes
+  int32_t* h_bad = nullptr;           // [kSlots] pinned: eviction-round consistency flag
+  ms::StepSizes* hd_sz = nullptr;     // device views of the two mailboxes
+  int32_t* hd_bad = nullptr;
   ms::RoundState* d_rs = nullptr;
   ms::RoundState* h_rs = nullptr;     // pinned mailbox
   ms::Counters* d_ctr = nullptr;
@@ -103,9 +108,10 @@ struct massive_ctx {
   int32_t* d_part = nullptr;
   int32_t* d_part2 = nullptr;
   int32_t* d_spart = nullptr;        // the sampler's scan partials (rounds use d_part, d_part2)
-  int2* d_hbm_list = nullptr;
-  int2* d_miss_list[2] = {};          // by step parity (read by the side stream)
-  int32_t* d_miss_slot[2] = {};       // per miss-list entry: write-through slot or -1
+  // gather lists by step slot (written by classify, read by the side stream)
+  int2* d_hbm_list[kSlots] = {};
+  int2* d_miss_list[kSlots] = {};
+  int32_t* d_miss_slot[kSlots] = {};  // per miss-list entry: write-through slot or -1
   uint8_t* d_dummy = nullptr;         // [row_bytes] row that idle copy lanes move onto itself
   int32_t* d_E = nullptr;
   int32_t* d_R = nullptr;
@@ -126,7 +132,7 @@ struct massive_ctx {
     int64_t step = -1;
     const int32_t* seeds = nullptr;
     int32_t n0 = 0;
-  } infl[2];
+  } infl[kSlots];
   // timing
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
@@ -366,19 +372,22 @@ void free_ctx(massive_ctx* c) {
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
-                 c->d_part, c->d_part2, c->d_spart, c->d_hbm_list, c->d_miss_list[0], c->d_miss_list[1], c->d_miss_slot[0],
-                 c->d_miss_slot[1], c->d_dummy, c->d_E, c->d_R,
+                 c->d_part, c->d_part2, c->d_spart, c->d_dummy, c->d_E, c->d_R,
                  c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
     if (p) (void)hipFree(p);
+  for (int i = 0; i < kSlots; ++i)
+    for (void* p : {(void*)c->d_hbm_list[i], (void*)c->d_miss_list[i], (void*)c->d_miss_slot[i]})
+      if (p) (void)hipFree(p);
   if (c->h_sz) (void)hipHostFree(c->h_sz);
   if (c->h_rs) (void)hipHostFree(c->h_rs);
   if (c->h_bad) (void)hipHostFree(c->h_bad);
   if (c->h_ctr) (void)hipHostFree(c->h_ctr);
-  for (hipEvent_t e : {c->ev_hbm_done[0], c->ev_hbm_done[1], c->ev_batch_done[0], c->ev_batch_done[1],
-                       c->ev_miss_done[0], c->ev_miss_done[1],
-                       c->ev_round_done, c->ev_refill_done})
+  for (int i = 0; i < kSlots; ++i)
+    for (hipEvent_t e : {c->ev_cls_done[i], c->ev_hbm_done[i], c->ev_batch_done[i], c->ev_miss_done[i]})
+      if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : {c->ev_round_done, c->ev_refill_done})
     if (e) (void)hipEventDestroy(e);
   for (auto& r : c->pending) {
     (void)hipEventDestroy(r.a);
@@ -438,9 +447,10 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
-  for (hipEvent_t* e : {&c->ev_hbm_done[0], &c->ev_hbm_done[1], &c->ev_batch_done[0], &c->ev_batch_done[1],
-                        &c->ev_miss_done[0], &c->ev_miss_done[1],
-                        &c->ev_round_done, &c->ev_refill_done})
+  for (int i = 0; i < kSlots; ++i)
+    for (hipEvent_t* e : {&c->ev_cls_done[i], &c->ev_hbm_done[i], &c->ev_batch_done[i], &c->ev_miss_done[i]})
+      CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+  for (hipEvent_t* e : {&c->ev_round_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
 
   // the pinned store must be mapped into the device address space
@@ -468,7 +478,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_pos_of, R * 4);
   CKA(c->d_big, R * 4);
   CKA(c->d_bits, (c->W + 4) * 4);
-  CKA(c->d_sz, 2 * sizeof(ms::StepSizes));
+  CKA(c->d_sz, kSlots * sizeof(ms::StepSizes));
   CKA(c->d_rs, sizeof(ms::RoundState));
   CKA(c->d_ctr, sizeof(ms::Counters));
   CKA(c->d_slot_round, cap * 4);
@@ -476,11 +486,11 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_part, c->pmax * 4);
   CKA(c->d_part2, c->pmax * 4);
   CKA(c->d_spart, c->pmax * 4);
-  CKA(c->d_hbm_list, R * 8);
-  CKA(c->d_miss_list[0], R * 8);
-  CKA(c->d_miss_list[1], R * 8);
-  CKA(c->d_miss_slot[0], R * 4);
-  CKA(c->d_miss_slot[1], R * 4);
+  for (int i = 0; i < kSlots; ++i) {
+    CKA(c->d_hbm_list[i], R * 8);
+    CKA(c->d_miss_list[i], R * 8);
+    CKA(c->d_miss_slot[i], R * 4);
+  }
   CKA(c->d_dummy, std::max<int64_t>(c->rb, 16));
   CKA(c->d_E, cap * 4);
   CKA(c->d_R, cap * 4);
@@ -491,11 +501,14 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_v1, c->sort_cap * 4);
   CKA(c->d_hist, 256 * cdiv(c->sort_cap, ms::kSortTile) * 4);
   CKA(c->d_ghist, 256 * 4);
-  if (hipHostMalloc((void**)&c->h_sz, 2 * sizeof(ms::StepSizes), hipHostMallocDefault) != hipSuccess ||
+  if (hipHostMalloc((void**)&c->h_sz, kSlots * sizeof(ms::StepSizes), hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_rs, sizeof(ms::RoundState), hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_bad, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_bad, kSlots * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_ctr, sizeof(ms::Counters), hipHostMallocDefault) != hipSuccess)
     return c->fail(MASSIVE_ENOMEM, "hipHostMalloc of the size mailboxes failed");
+  if (hipHostGetDevicePointer((void**)&c->hd_sz, c->h_sz, 0) != hipSuccess || !c->hd_sz ||
+      hipHostGetDevicePointer((void**)&c->hd_bad, c->h_bad, 0) != hipSuccess || !c->hd_bad)
+    return c->fail(MASSIVE_EHIP, "the size mailboxes have no device view");
 
   hipStream_t s = c->s_main;
   CK(hipMemcpyAsync(c->d_indptr, a->indptr, (R + 1) * 8, hipMemcpyHostToDevice, s));
@@ -546,9 +559,10 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
     CK(hipMemcpyAsync(&c->d_rs->k, &c->h_rs->k, 8, hipMemcpyHostToDevice, s));
     launch_refill(c, s, &c->d_rs->k, cap, 0, 0, 1);
   }
-  // the step-parity events start out complete
-  for (int i = 0; i < 2; ++i) {
-    CK(hipEventRecord(c->ev_hbm_done[i], s));
+  // the step-slot events start out complete
+  for (int i = 0; i < kSlots; ++i) {
+    CK(hipEventRecord(c->ev_cls_done[i], s));
+    CK(hipEventRecord(c->ev_hbm_done[i], c->s_miss));
     CK(hipEventRecord(c->ev_batch_done[i], c->s_miss));
     CK(hipEventRecord(c->ev_miss_done[i], c->s_miss));
   }
@@ -615,9 +629,11 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   if (!io || n0 < 0 || (n0 > 0 && !seeds)) return c->fail(MASSIVE_EINVAL, "bad seeds / batch arguments");
   if (c->pending_round) return c->fail(MASSIVE_ESTATE, "massive_evict_step was not called after the last step");
   if (n0 > c->L) return c->fail(MASSIVE_EINVAL, "more seeds than local nodes");
-  const int slot = (int)(c->t & 1);
-  if (c->infl[slot].io) return c->fail(MASSIVE_ESTATE, "two batches in flight: wait for the older one first");
-  if (c->infl[slot ^ 1].io == io) return c->fail(MASSIVE_ESTATE, "this batch is still in flight");
+  const int slot = (int)(c->t % kSlots);
+  if (c->infl[slot].io)
+    return c->fail(MASSIVE_ESTATE, "%d batches in flight: wait for the oldest one first", kSlots);
+  for (int i = 0; i < kSlots; ++i)
+    if (c->infl[i].io == io) return c->fail(MASSIVE_ESTATE, "this batch is still in flight");
   int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
   massive_output_bounds(c, n0, nb, eb);
   if (!io->nodes || !io->mask || !io->feat) return c->fail(MASSIVE_EINVAL, "nodes / mask / feat are NULL");
@@ -648,7 +664,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   ms::StepSizes* sz = c->d_sz + slot;
   int2* miss_list = c->d_miss_list[slot];
   const uint32_t key0 = (uint32_t)c->seed, key1 = (uint32_t)(c->seed >> 32);
-  // this parity's sizes and miss list were last used by the side stream two
+  // this slot's sizes and lists were last used by the side stream kSlots
   // steps ago (complete: that batch was waited for)
   CK(hipStreamWaitEvent(s, c->ev_batch_done[slot], 0));
   CK(hipMemsetAsync(sz, 0, sizeof(ms::StepSizes), s));
@@ -737,7 +753,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ca.S_A = c->d_S_A;
     ca.pos_of = c->d_pos_of;
     ca.mask = io->mask;
-    ca.hbm_list = c->d_hbm_list;
+    ca.hbm_list = c->d_hbm_list[slot];
     ca.miss_list = miss_list;
     ca.miss_slot = c->d_miss_slot[slot];
     ca.slot_round = c->d_slot_round;
@@ -746,35 +762,36 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, 4096), ms::kClsNT, 0, s>>>(ca);
   }
   if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of, sz);
-  // HBM rows first, at full bandwidth; the host-link rows follow on the side
-  // stream (concurrent host reads would throttle the HBM gather) and overlap
-  // whatever the main stream does next.
-  // no host-link reads while the HBM gather runs: the previous step's miss
-  // gather and the last refill chunk finish first
-  CK(hipStreamWaitEvent(s, c->ev_miss_done[slot ^ 1], 0));
-  if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
-  launch_gather(c, 2, kHbm, s, c->d_hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
+  CK(hipEventRecord(c->ev_cls_done[slot], s));
+  // The gathers run on the side stream, so the main stream goes on to the
+  // next step's sampling at once. HBM rows first, at full bandwidth: after the
+  // previous step's miss gather (stream order) and the last refill chunk, as
+  // concurrent host-link reads would throttle them; then the host-link rows,
+  // beside the refill chunk launched after the HBM gather.
+  hipStream_t sm = c->s_miss;
+  CK(hipStreamWaitEvent(sm, c->ev_cls_done[slot], 0));
+  if (c->refill_inflight) CK(hipStreamWaitEvent(sm, c->ev_refill_done, 0));
+  launch_gather(c, 2, kHbm, sm, c->d_hbm_list[slot], &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
                 c->hbm_blocks);
-  CK(hipEventRecord(c->ev_hbm_done[slot], s));
+  CK(hipEventRecord(c->ev_hbm_done[slot], sm));
   {
     int rc = launch_refill_chunks(c, 1, c->ev_hbm_done[slot]);
     if (rc != MASSIVE_OK) return rc;
   }
-  CK(hipStreamWaitEvent(c->s_miss, c->ev_hbm_done[slot], 0));
   if (c->H > 0) {
-    launch_gather(c, 3, kMiss, c->s_miss, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
+    launch_gather(c, 3, kMiss, sm, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
                   c->host_blocks, c->d_miss_slot[slot], c->d_slab + (int64_t)c->L * c->rb);
   }
-  CK(hipEventRecord(c->ev_miss_done[slot], c->s_miss));
-  if (c->H > 0) {
-    // rows written through into their slots are landed from here on
-    if (pend >= 0)
-      ms::k_publish<<<grid_for(nb[c->K], 256, 1024), 256, 0, c->s_miss>>>(c->d_miss_slot[slot], &sz->n_miss,
-                                                                          c->d_landed, c->cap, pend);
+  CK(hipEventRecord(c->ev_miss_done[slot], sm));
+  // rows written through into their slots are landed from here on; the
+  // step's sizes go to the host mailbox
+  {
+    const bool publish = pend >= 0 && c->H > 0;
+    ms::k_step_done<<<publish ? grid_for(nb[c->K], 256, 1024) : 1, 256, 0, sm>>>(
+        c->d_miss_slot[slot], &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, &c->d_ctr->bad,
+        c->hd_sz + slot, c->hd_bad + slot);
   }
-  CK(hipMemcpyAsync(c->h_sz + slot, sz, sizeof(ms::StepSizes), hipMemcpyDeviceToHost, c->s_miss));
-  CK(hipMemcpyAsync(c->h_bad + slot, &c->d_ctr->bad, sizeof(int32_t), hipMemcpyDeviceToHost, c->s_miss));
-  CK(hipEventRecord(c->ev_batch_done[slot], c->s_miss));
+  CK(hipEventRecord(c->ev_batch_done[slot], sm));
   CK(hipGetLastError());
   c->infl[slot].io = io;
   c->infl[slot].step = c->t;
@@ -788,7 +805,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
 int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   if (!c || !io) return MASSIVE_EINVAL;
   int slot = -1;
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < kSlots; ++i)
     if (c->infl[i].io == io) slot = i;
   if (slot < 0) return c->fail(MASSIVE_EINVAL, "this batch is not in flight");
   const massive_ctx::InFlight f = c->infl[slot];
@@ -803,7 +820,9 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
     // the step left no trace on the device; it can be taken back if nothing
     // was issued after it
     const char* why = (z.status & 1) ? "a seed is not a local node id" : "a seed is repeated";
-    if (f.step == c->t - 1 && c->pending_round && !c->infl[slot ^ 1].io) {
+    bool alone = true;
+    for (int i = 0; i < kSlots; ++i) alone = alone && !c->infl[i].io;
+    if (f.step == c->t - 1 && c->pending_round && alone) {
       c->t -= 1;
       c->pending_round = false;
       return c->fail(MASSIVE_EINVAL, "%s", why);
@@ -856,7 +875,7 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     if (rc != MASSIVE_OK) return rc;
   }
   c->round_pending_rows = false;
-  CK(hipStreamWaitEvent(s, c->ev_hbm_done[tl & 1], 0));
+  CK(hipStreamWaitEvent(s, c->ev_hbm_done[tl % kSlots], 0));
   {
     massive_ctx::Range tr(c, s, 4);
     ms::k_materialize<<<grid_for(cap, 256), 256, 0, s>>>(c->d_S_E, c->d_hitcnt, cap, (int32_t)(c->t - c->mat_t),
@@ -908,7 +927,7 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   // the refill is copied in chunks after the next steps' HBM gathers; the last
   // step's miss gather may still write rows of the previous round's
   // replacements into slots this round reassigns, so the new refill comes after it
-  CK(hipStreamWaitEvent(s, c->ev_batch_done[tl & 1], 0));
+  CK(hipStreamWaitEvent(s, c->ev_miss_done[tl % kSlots], 0));
   c->chunks_left = c->refill_chunks;
   c->round_pending_rows = true;
   CK(hipGetLastError());

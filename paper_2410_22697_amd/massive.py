@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libmassive.so")
 MAX_HOPS = 8
 
 OK, EINVAL, ECAPACITY, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
+MAX_INFLIGHT = 3  # batches enqueued with sample_async and not yet waited for
 _NAMES = {EINVAL: "EINVAL", ECAPACITY: "ECAPACITY", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE"}
 
 EXPORTS = ("massive_init", "massive_output_bounds", "massive_sample", "massive_sample_async",

@@ -22,6 +22,16 @@ def test_header_declares_the_three_calls():
         assert n in names
 
 
+def test_binding_constants_match_the_header():
+    from paper_2410_22697_amd import massive
+    text = open(HEADER).read()
+    defs = dict(re.findall(r"#define (MASSIVE_[A-Z_]+) \(?(-?\d+)\)?", text))
+    assert int(defs["MASSIVE_MAX_HOPS"]) == massive.MAX_HOPS
+    assert int(defs["MASSIVE_MAX_INFLIGHT"]) == massive.MAX_INFLIGHT
+    for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE"):
+        assert int(defs["MASSIVE_" + name]) == getattr(massive, name), name
+
+
 def test_library_exports_every_declared_symbol():
     from paper_2410_22697_amd import massive
     if not os.path.exists(massive.LIB_PATH):

@@ -1,5 +1,5 @@
-"""GPU parity of the look-ahead pipeline: massive_sample_async with two batches
-in flight and eviction rounds enqueued without waiting, against the oracle
+"""GPU parity of the look-ahead pipeline: massive_sample_async with two or three
+batches in flight and eviction rounds enqueued without waiting, against the oracle
 run step by step. With a short eviction interval on the products-sized graph
 the refills (hundreds of thousands of rows over the host link) are still in
 flight when the next steps classify, so hits on refilled slots are served
@@ -19,13 +19,17 @@ def _gpu():
     require_gpu()
 
 
-def run_lookahead(name, prob, seeds_of, steps):
+def run_lookahead(name, prob, seeds_of, steps, depth=None):
+    """Steps 0..steps-1 with `depth` batches in flight (step t is enqueued
+    before step t - depth + 1 is waited for)."""
     import torch
+    from paper_2410_22697_amd import MAX_INFLIGHT
+    depth = depth or MAX_INFLIGHT
     orc = prob.oracle()
     gm = make_gpu(prob)
     K = len(prob.fanout)
     batch_max = max(len(seeds_of(t)) for t in range(steps))
-    bbs = [gm.alloc_batch(batch_max), gm.alloc_batch(batch_max)]
+    bbs = [gm.alloc_batch(batch_max) for _ in range(depth)]
     cap = gm.cap
     outs = [tuple(torch.full((max(cap, 1),), -7, dtype=torch.int32, device="cuda") for _ in range(3))
             for _ in range(steps)]
@@ -34,22 +38,22 @@ def run_lookahead(name, prob, seeds_of, steps):
     pending = []
 
     def check(t):
-        res = gm.wait(bbs[t % 2])
+        res = gm.wait(bbs[t % depth])
         pending.append(res.host_rows - res.misses)
         st = orc.sample(seeds_of(t))
-        compare_step("%s t=%d" % (name, t), st, res, bbs[t % 2], K)
+        compare_step("%s t=%d" % (name, t), st, res, bbs[t % depth], K)
         ro = orc.evict_step()
         rounds_o.append(ro)
         return ro.k
 
     for t in range(steps):
         log("%s t=%d enqueue" % (name, t))
-        gm.sample_async(seeds_dev[t], bbs[t % 2])
+        gm.sample_async(seeds_dev[t], bbs[t % depth])
         gm.evict_step(outs[t], wait=False)
-        if t >= 1:
-            k = check(t - 1)
-            evicted_o += k
-    evicted_o += check(steps - 1)
+        if t >= depth - 1:
+            evicted_o += check(t - depth + 1)
+    for t in range(max(0, steps - depth + 1), steps):
+        evicted_o += check(t)
     torch.cuda.synchronize()
     n_rounds = 0
     for t, ro in enumerate(rounds_o):
@@ -67,9 +71,10 @@ def run_lookahead(name, prob, seeds_of, steps):
     return n_rounds, sum(pending)
 
 
-def test_lookahead_cl10k():
+@pytest.mark.parametrize("depth", [2, 3])
+def test_lookahead_cl10k(depth):
     prob, sched, w = workload_problem("cl10k", delta=3, gamma=0.8)
-    assert run_lookahead("async cl10k", prob, sched.seeds, 24)[0] >= 3
+    assert run_lookahead("async cl10k depth %d" % depth, prob, sched.seeds, 24, depth)[0] >= 3
 
 
 def test_lookahead_cl2m45_inflight_refills():
@@ -78,21 +83,26 @@ def test_lookahead_cl2m45_inflight_refills():
     assert rounds == 2 and pending > 0  # hits on refilling slots were written through
 
 
-def test_lookahead_rejects_a_third_batch():
-    from paper_2410_22697_amd import MassiveError
+def test_lookahead_rejects_one_batch_too_many():
+    from paper_2410_22697_amd import MAX_INFLIGHT, MassiveError
     prob, sched, w = workload_problem("cl10k")
     gm = make_gpu(prob)
-    bbs = [gm.alloc_batch(w.batch) for _ in range(3)]
-    s = [to_dev(sched.seeds(t)) for t in range(3)]
-    gm.sample_async(s[0], bbs[0])
-    gm.evict_step(wait=False)
-    gm.sample_async(s[1], bbs[1])
-    gm.evict_step(wait=False)
+    n = MAX_INFLIGHT + 1
+    bbs = [gm.alloc_batch(w.batch) for _ in range(n)]
+    s = [to_dev(sched.seeds(t)) for t in range(n)]
+    for t in range(MAX_INFLIGHT):
+        gm.sample_async(s[t], bbs[t])
+        gm.evict_step(wait=False)
     with pytest.raises(MassiveError) as ei:
-        gm.sample_async(s[2], bbs[2])
+        gm.sample_async(s[n - 1], bbs[n - 1])
     assert ei.value.code == -5
+    # a batch still in flight cannot be enqueued again either
     gm.wait(bbs[0])
-    gm.wait(bbs[1])
+    with pytest.raises(MassiveError) as ei:
+        gm.sample_async(s[n - 1], bbs[1])
+    assert ei.value.code == -5
+    for t in range(1, MAX_INFLIGHT):
+        gm.wait(bbs[t])
 
 
 # Rows of 4, 8, 12, 16, 100 and 4000 bytes (fp32) and 4 and 100 bytes (bf16):
