@@ -80,7 +80,8 @@ struct ClassifyArgs {
   const uint64_t* tab;
   uint32_t tmask;
   int32_t* hitcnt;
-  float* S_A;
+  float* S_A;                 // by halo rank
+  const int32_t* rank_of;     // halo id -> rank
   int32_t* pos_of;
   uint8_t* mask;
   int2* hbm_list;
@@ -100,8 +101,9 @@ constexpr int kClsItems = 8;  // rows per thread: one block classifies 2048 rows
 // frontier ids; a window of four table entries from each id's probe start
 // (the 16-byte pairs holding entries p & ~1 .. (p & ~1) + 3, which settle
 // almost every search; the rare rest probes on one by one); the hit slots'
-// counters and refill stamps. Lanes past the end and local rows load dummy
-// (in-range) addresses and change nothing.
+// counters and refill stamps (and the misses' ranks: S_A is kept by rank).
+// Lanes past the end and local rows load dummy (in-range) addresses and
+// change nothing.
 __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   constexpr int NW = kClsNT / MS_WAVE;
   __shared__ int32_t wc[NW][4];          // per-wave counts: hbm list, host list, local, pending hits
@@ -152,11 +154,12 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
         slot[it] = r;
       }
     }
-    int32_t hc[kClsItems], sr[kClsItems], ld[kClsItems];
+    int32_t hc[kClsItems], sr[kClsItems], ld[kClsItems], rk[kClsItems];
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
       const int32_t sl = slot[it] >= 0 ? slot[it] : 0;
       hc[it] = a.hitcnt[sl];
+      rk[it] = a.rank_of[v[it] >= a.L && slot[it] < 0 ? v[it] - a.L : 0];
       sr[it] = 0;
       ld[it] = 0;
       if (pending) {  // the same in every lane
@@ -169,6 +172,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
       pin(hc[it]);
       pin(sr[it]);
       pin(ld[it]);
+      pin(rk[it]);
     }
     int cls[kClsItems];
     int32_t src[kClsItems], wslot[kClsItems];
@@ -199,7 +203,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
         } else {
           cls[it] = 2;
           src[it] = h;
-          atomicAdd(&a.S_A[h], 1.0f);
+          atomicAdd(&a.S_A[rk[it]], 1.0f);
         }
         a.mask[i] = (uint8_t)(cls[it] == 3 ? 1 : cls[it]);
       }
@@ -539,6 +543,11 @@ __global__ void k_fill_gated(T* __restrict__ p, int64_t n, T v, const int64_t* _
 // key T of the k'-th candidate and how many candidates with key T to take.
 __device__ __forceinline__ uint32_t cand_key(float a) { return ~__float_as_uint(a); }
 
+// One radix-select pass over the candidate keys (S_A >= 0, by rank) that
+// match the prefix so far. Each thread takes four consecutive scores per
+// iteration (one 16-byte load); a wave adds the lanes whose digit equals its
+// first active lane's with one LDS atomic (most candidates have S_A = 0, one
+// digit), the others one by one.
 __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S_A, int64_t H,
                                                      const RoundState* __restrict__ rs, int shift,
                                                      uint32_t* __restrict__ ghist) {
@@ -547,11 +556,34 @@ __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S
   hist[threadIdx.x] = 0;
   __syncthreads();
   const uint32_t prefix = rs->prefix, pmask = rs->pmask;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < H; i += (int64_t)gridDim.x * blockDim.x) {
-    const float a = S_A[i];
-    if (a >= 0.0f) {
-      const uint32_t k = cand_key(a);
-      if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+  const int lane = lane_id();
+  const int64_t H4 = H / 4;
+  const float4* S4 = reinterpret_cast<const float4*>(S_A);
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < (H + 3) / 4;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    float a[4] = {-1.0f, -1.0f, -1.0f, -1.0f};
+    if (q < H4) {
+      const float4 x = S4[q];
+      a[0] = x.x;
+      a[1] = x.y;
+      a[2] = x.z;
+      a[3] = x.w;
+    } else {
+      for (int j = 0; j < 4; ++j)
+        if (4 * q + j < H) a[j] = S_A[4 * q + j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t k = cand_key(a[j]);
+      const bool in = a[j] >= 0.0f && (k & pmask) == prefix;
+      const uint32_t d = (k >> shift) & 255u;
+      const uint64_t m = ballot(in);
+      if (!m) continue;
+      const int first = __ffsll((unsigned long long)m) - 1;
+      const uint32_t d0 = __shfl(d, first, MS_WAVE);
+      const uint64_t same = ballot(in && d == d0);
+      if (lane == first) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+      else if (in && d != d0) atomicAdd(&hist[d], 1u);
     }
   }
   __syncthreads();
@@ -592,26 +624,28 @@ __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs
 }
 
 // In rank order r: candidates with key < T go to (keys, vals) for sorting,
-// the first `need` with key == T go straight to R[n_lt + ...].
-__global__ __launch_bounds__(kScanNT) void k_rank_count(const float* __restrict__ S_A,
-                                                        const int32_t* __restrict__ h_of_rank, int64_t H,
+// the first `need` with key == T go straight to R[n_lt + ...]. S_A is kept by
+// rank, so both passes read it (and h_of_rank) in order.
+__global__ __launch_bounds__(kScanNT) void k_rank_count(const float* __restrict__ S_A, int64_t H,
                                                         RoundState* __restrict__ rs,
                                                         int32_t* __restrict__ p_lt, int32_t* __restrict__ p_eq) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   const uint32_t T = rs->prefix;
   const bool on = rs->k > 0;
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
-  int32_t clt = 0, ceq = 0;
+  float a[kScanItems];
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     const int64_t r = base + (int64_t)it * kScanNT + threadIdx.x;
-    if (on && r < H) {
-      const float a = S_A[h_of_rank[r]];
-      if (a >= 0.0f) {
-        const uint32_t k = cand_key(a);
-        clt += k < T;
-        ceq += k == T;
-      }
+    a[it] = on && r < H ? S_A[r] : -1.0f;
+  }
+  int32_t clt = 0, ceq = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    if (a[it] >= 0.0f) {
+      const uint32_t k = cand_key(a[it]);
+      clt += k < T;
+      ceq += k == T;
     }
   }
   clt = block_sum<kScanNT>(clt, lds);
@@ -637,22 +671,21 @@ __global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__
   const int64_t need = rs->need, n_lt = rs->k - rs->need;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   uint32_t k[kScanItems];
+  float a[kScanItems];
   int32_t h[kScanItems];
   bool lt[kScanItems], eq[kScanItems];
   int32_t clt = 0, ceq = 0;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     const int64_t r = base + it;
-    lt[it] = eq[it] = false;
-    if (r < H) {
-      h[it] = h_of_rank[r];
-      const float a = S_A[h[it]];
-      if (a >= 0.0f) {
-        k[it] = cand_key(a);
-        lt[it] = k[it] < T;
-        eq[it] = k[it] == T;
-      }
-    }
+    a[it] = r < H ? S_A[r] : -1.0f;
+    h[it] = r < H ? h_of_rank[r] : -1;
+  }
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    k[it] = cand_key(a[it]);
+    lt[it] = a[it] >= 0.0f && k[it] < T;
+    eq[it] = a[it] >= 0.0f && k[it] == T;
     clt += lt[it];
     ceq += eq[it];
   }
@@ -672,6 +705,13 @@ __global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__
       ++oeq;
     }
   }
+}
+
+// S_A by halo id from S_A by rank (for export).
+__global__ void k_scores_by_id(const float* __restrict__ S_A, const int32_t* __restrict__ h_of_rank, int64_t H,
+                               float* __restrict__ out) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < H; r += (int64_t)gridDim.x * blockDim.x)
+    out[h_of_rank[r]] = S_A[r];
 }
 
 // ------------------------------------------------------ stable radix sort
@@ -812,7 +852,7 @@ __global__ void k_rank_finish(const int32_t* __restrict__ h_of_rank, int64_t H, 
     rank_of[h_of_rank[r]] = (int32_t)r;
 }
 
-// Initial buffer: slot s holds the halo node of rank s.
+// Initial buffer: slot s holds the halo node of rank s (S_A is by rank).
 __global__ void k_init_buffer(const int32_t* __restrict__ h_of_rank, int64_t cap, int32_t L,
                               int32_t* __restrict__ slot_id, float* __restrict__ S_E, int32_t* __restrict__ hitcnt,
                               float* __restrict__ S_A, int2* __restrict__ fill) {
@@ -821,7 +861,7 @@ __global__ void k_init_buffer(const int32_t* __restrict__ h_of_rank, int64_t cap
     slot_id[s] = h;
     S_E[s] = 1.0f;
     hitcnt[s] = 0;
-    S_A[h] = -1.0f;
+    S_A[s] = -1.0f;
     fill[s] = make_int2((int32_t)(L + s), h);
   }
 }
@@ -853,10 +893,11 @@ __global__ void k_esel_keys_slot(const int32_t* __restrict__ vals, const int64_t
 // ------------------------------------------------------------------ swap
 // Pair E[i] (ascending slot) with R[i]; every read sees pre-round values
 // because the slots, the evicted nodes and the replacements are all
-// distinct, so no two threads touch the same entry.
+// distinct, so no two threads touch the same entry. S_A is by rank.
 __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict__ R, const int64_t* __restrict__ k_ptr,
                        int32_t L, int64_t cap, int32_t H, int32_t* __restrict__ slot_id, float* __restrict__ S_E,
-                       float* __restrict__ S_A, int32_t* __restrict__ out_ev, int32_t* __restrict__ out_slot,
+                       float* __restrict__ S_A, const int32_t* __restrict__ rank_of,
+                       int32_t* __restrict__ out_ev, int32_t* __restrict__ out_slot,
                        int32_t* __restrict__ out_rep, int2* __restrict__ fill, int32_t* __restrict__ bad,
                        int32_t* __restrict__ slot_round, int32_t round_id) {
   const int64_t k = *k_ptr;
@@ -868,10 +909,11 @@ __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict_
       continue;
     }
     const int32_t e = slot_id[s];
-    const float se = S_E[s], sa = S_A[r];
-    S_A[e] = se;
+    const int32_t re = rank_of[e], rr = rank_of[r];
+    const float se = S_E[s], sa = S_A[rr];
+    S_A[re] = se;
     S_E[s] = sa;
-    S_A[r] = -1.0f;
+    S_A[rr] = -1.0f;
     slot_id[s] = r;
     slot_round[s] = round_id;
     if (out_ev) out_ev[i] = e;

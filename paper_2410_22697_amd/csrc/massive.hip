@@ -751,6 +751,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ca.tmask = c->hmask;
     ca.hitcnt = c->d_hitcnt;
     ca.S_A = c->d_S_A;
+    ca.rank_of = c->d_rank_of;
     ca.pos_of = c->d_pos_of;
     ca.mask = io->mask;
     ca.hbm_list = c->d_hbm_list[slot];
@@ -906,14 +907,14 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
       ms::k_select_pick<<<1, 256, 0, s>>>(rs, c->d_ghist, shift, &c->d_ctr->bad);
     }
     const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
-    ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2);
+    ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, H, rs, c->d_part, c->d_part2);
     ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2,
                                                           c->d_k0, c->d_v0, c->d_R);
     // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
     sort_u32(c, s, &rs->n_lt, 0, cap, c->d_R);
     c->round_id += 1;
     ms::k_swap<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, c->d_R, &rs->k, c->L, cap, c->H, c->d_slot_id, c->d_S_E,
-                                                  c->d_S_A, evicted, slots, replaced, c->d_fill, &c->d_ctr->bad,
+                                                  c->d_S_A, c->d_rank_of, evicted, slots, replaced, c->d_fill, &c->d_ctr->bad,
                                                   c->d_slot_round, c->round_id);
     ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
@@ -965,7 +966,13 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
   }
   if (slot_id && c->cap) CK(hipMemcpyAsync(slot_id, c->d_slot_id, c->cap * 4, hipMemcpyDeviceToHost, s));
   if (S_E && c->cap) CK(hipMemcpyAsync(S_E, c->d_S_E, c->cap * 4, hipMemcpyDeviceToHost, s));
-  if (S_A && c->H) CK(hipMemcpyAsync(S_A, c->d_S_A, (int64_t)c->H * 4, hipMemcpyDeviceToHost, s));
+  if (S_A && c->H) {
+    // S_A is kept by halo rank; export it by halo id (through a sort buffer,
+    // free once the last round has completed)
+    float* by_id = reinterpret_cast<float*>(c->d_v1);
+    ms::k_scores_by_id<<<grid_for(c->H, 256), 256, 0, s>>>(c->d_S_A, c->d_h_of_rank, c->H, by_id);
+    CK(hipMemcpyAsync(S_A, by_id, (int64_t)c->H * 4, hipMemcpyDeviceToHost, s));
+  }
   CK(hipStreamSynchronize(s));
   if (t) *t = c->t;
   return MASSIVE_OK;
