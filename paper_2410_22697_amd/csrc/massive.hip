@@ -107,7 +107,9 @@ struct massive_ctx {
   int32_t* d_landed = nullptr;        // [cap] round whose refill row has landed
   int32_t* d_part = nullptr;
   int32_t* d_part2 = nullptr;
-  int32_t* d_spart = nullptr;        // the sampler's scan partials (rounds use d_part, d_part2)
+  uint64_t* d_scan_flags = nullptr;  // the sampler's single-pass scans (rounds use d_part, d_part2)
+  int64_t scan_tiles = 0;
+  uint32_t scan_epoch = 0;           // of the last scan launched
   // gather lists by step slot (written by classify, read by the side stream)
   int2* d_hbm_list[kSlots] = {};
   int2* d_miss_list[kSlots] = {};
@@ -372,7 +374,7 @@ void free_ctx(massive_ctx* c) {
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
-                 c->d_part, c->d_part2, c->d_spart, c->d_dummy, c->d_E, c->d_R,
+                 c->d_part, c->d_part2, c->d_scan_flags, c->d_dummy, c->d_E, c->d_R,
                  c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
                  c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
   for (void* p : dev)
@@ -485,7 +487,8 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_landed, cap * 4);
   CKA(c->d_part, c->pmax * 4);
   CKA(c->d_part2, c->pmax * 4);
-  CKA(c->d_spart, c->pmax * 4);
+  c->scan_tiles = std::max(cdiv(R, ms::kScanTile), cdiv(c->W, ms::kScanTile)) + 1;
+  CKA(c->d_scan_flags, c->scan_tiles * 8);
   for (int i = 0; i < kSlots; ++i) {
     CKA(c->d_hbm_list[i], R * 8);
     CKA(c->d_miss_list[i], R * 8);
@@ -527,6 +530,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CK(hipMemsetAsync(c->d_pos_of, 0xFF, R * 4, s));
   CK(hipMemsetAsync(c->d_bits, 0, (c->W + 4) * 4, s));
   CK(hipMemsetAsync(c->d_ghist, 0, 256 * 4, s));
+  CK(hipMemsetAsync(c->d_scan_flags, 0, c->scan_tiles * 8, s));
   CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
   CK(hipMemsetAsync(c->d_slot_round, 0xFF, cap * 4, s));
   CK(hipMemsetAsync(c->d_landed, 0xFF, cap * 4, s));
@@ -623,6 +627,16 @@ int massive_output_bounds(const massive_ctx* c, int32_t n_seeds, int64_t* n_boun
   return MASSIVE_OK;
 }
 
+// The epoch of the next single-pass scan (flags of earlier epochs are stale
+// by their tag); the flags are cleared before the tags could wrap around.
+uint32_t next_scan_epoch(massive_ctx* c, hipStream_t s) {
+  if (c->scan_epoch >= (1u << 30)) {
+    ms::k_fill<uint64_t><<<grid_for(c->scan_tiles, 256), 256, 0, s>>>(c->d_scan_flags, c->scan_tiles, 0ull);
+    c->scan_epoch = 0;
+  }
+  return ++c->scan_epoch;
+}
+
 int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
   if (!c) return MASSIVE_EINVAL;
   if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier failure");
@@ -677,10 +691,9 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
       // the previous hop's relabel shares the launch
       const int64_t nrel = k > 1 ? (int64_t)grid_for(eb[k - 2], ms::kScanTile, 1024) : 0;
-      ms::k_row_counts<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
-          c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], c->d_spart, c->d_big, c->big_min, nbk,
-          k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
-      ms::k_row_offsets<<<(unsigned)nbk, ms::kScanNT, 0, s>>>(sz, k, io->indptr[k - 1], c->d_spart);
+      ms::k_row_scan<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
+          c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], c->d_scan_flags, next_scan_epoch(c, s),
+          c->d_big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;
@@ -713,9 +726,8 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
                              ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
       }
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_count<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart);
-      ms::k_bits_emit<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_spart, io->nodes,
-                                                             c->d_pos_of);
+      ms::k_bits_scan<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_scan_flags,
+                                                             next_scan_epoch(c, s), io->nodes, c->d_pos_of);
       if (k == c->K)
         ms::k_relabel<<<grid_for(eb[k - 1], ms::kScanTile, 1024), ms::kScanNT, 0, s>>>(io->indices[k - 1], sz, k,
                                                                                      c->d_pos_of);
@@ -833,7 +845,9 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   }
   if (z.status) {
     c->broken = true;
-    return c->fail(MASSIVE_EHIP, "sampler could not isolate a candidate set (status %d)", z.status);
+    return c->fail(MASSIVE_EHIP, "%s (status %d)",
+                   (z.status & 8) ? "a single-pass scan waited past its bound" : "sampler could not isolate a candidate set",
+                   z.status);
   }
   for (int k = 0; k <= c->K; ++k) io->n[k] = z.n[k];
   for (int k = 0; k < c->K; ++k) io->e[k] = z.e[k];

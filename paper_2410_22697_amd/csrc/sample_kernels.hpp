@@ -21,6 +21,61 @@ __device__ __forceinline__ int32_t preceding_sum(const int32_t* __restrict__ par
   return block_sum<NT>(s, lds);
 }
 
+// Single-pass scan by decoupled look-back: tile b publishes its aggregate,
+// then its inclusive prefix once the tiles before it are known. flags[b] =
+// tag << 32 | value, tag = 2 * epoch (aggregate) or 2 * epoch + 1 (inclusive
+// prefix); the epoch differs for every launch, so flags are never cleared.
+// Tiles are blocks in blockIdx order. Each XCD dispatches its blocks in
+// order, so the lowest unfinished tile is always resident and every wait
+// ends. The wait is bounded all the same: past the limit the step is flagged
+// (status bit 8) and the tile goes on with the values it has.
+constexpr int kLookbackSpins = 1 << 20;
+
+__device__ __forceinline__ uint32_t lookback_exclusive(uint64_t* flags, int64_t b, uint32_t agg, uint32_t epoch,
+                                                       int32_t* status, uint32_t* excl_lds) {
+  const uint32_t t_agg = 2u * epoch, t_inc = 2u * epoch + 1u;
+  if (wave_id() == 0) {
+    const int lane = lane_id();
+    if (lane == 0)
+      __hip_atomic_store(&flags[b], ((uint64_t)(b == 0 ? t_inc : t_agg) << 32) | agg, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t excl = 0;
+    int64_t p = b - 1;  // the window is tiles p - 63 .. p, lane l on tile p - l
+    int spins = 0;
+    while (p >= 0) {
+      const int64_t i = p - lane;
+      // before tile 0: an inclusive prefix of zero
+      const uint64_t f = i >= 0 ? __hip_atomic_load(&flags[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                : ((uint64_t)t_inc << 32);
+      const uint32_t tag = (uint32_t)(f >> 32);
+      const uint64_t ready = ballot(tag == t_agg || tag == t_inc);
+      const uint64_t inc = ballot(tag == t_inc);
+      // lanes 0..k must be ready, k = the nearest inclusive prefix (or the window)
+      const int k = inc ? __ffsll((unsigned long long)inc) - 1 : MS_WAVE - 1;
+      const uint64_t need = k == MS_WAVE - 1 ? ~0ull : ((2ull << k) - 1);
+      if ((ready & need) == need) {
+        excl += wave_sum(lane <= k ? (uint32_t)f : 0u);
+        if (inc) break;
+        p -= MS_WAVE;
+        continue;
+      }
+      if (++spins > kLookbackSpins) {
+        if (lane == 0) atomicOr(status, 8);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (lane == 0) {
+      if (b > 0)
+        __hip_atomic_store(&flags[b], ((uint64_t)t_inc << 32) | (excl + agg), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      *excl_lds = excl;
+    }
+  }
+  __syncthreads();
+  return *excl_lds;
+}
+
 // ---------------------------------------------------------------- seeds
 // F_0 = seeds; pos_of[seed] = its position. Flags out-of-range or repeated
 // seeds in sz->status (the step is then abandoned by every later kernel).
@@ -51,9 +106,10 @@ __global__ void k_seed_undo(const int32_t* __restrict__ seeds, int32_t n0, int32
 }
 
 // ------------------------------------------------------ per-row counts + scan
-// Block b < nbk: sum over its tile of min(deg(F[i]), fo); counts go to
-// bptr[i+1], rows longer than big_min to big_rows (one global atomic per
-// block). Every load of a thread is issued before the first is used.
+// Block b < nbk: the rows of tile b get min(deg(F[i]), fo) positions; the
+// tile's exclusive prefix comes from the single-pass scan, and bptr[0..n]
+// gets the offsets. Rows longer than big_min go to big_rows (one global atomic
+// per block). Every load of a thread is issued before the first is used.
 // Blocks b >= nbk relabel the previous hop's sampled ids (rel_ids, if given):
 // that work depends on the same kernels and shares the launch.
 __device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t e, const int32_t* __restrict__ pos_of,
@@ -81,36 +137,33 @@ __device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t
   }
 }
 
-__global__ __launch_bounds__(kScanNT) void k_row_counts(const int64_t* __restrict__ csr_indptr,
-                                                        const int32_t* __restrict__ nodes,
-                                                        StepSizes* sz, int hop, int32_t fo,
-                                                        int32_t* __restrict__ bptr,
-                                                        int32_t* __restrict__ partials,
-                                                        int32_t* __restrict__ big_rows, int64_t big_min, int64_t nbk,
-                                                        int32_t* __restrict__ rel_ids,
-                                                        const int32_t* __restrict__ pos_of) {
+__global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict__ csr_indptr,
+                                                      const int32_t* __restrict__ nodes, StepSizes* sz, int hop,
+                                                      int32_t fo, int32_t* __restrict__ bptr, uint64_t* flags,
+                                                      uint32_t epoch, int32_t* __restrict__ big_rows,
+                                                      int64_t big_min, int64_t nbk, int32_t* __restrict__ rel_ids,
+                                                      const int32_t* __restrict__ pos_of) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   __shared__ int32_t big_lds[kScanTile];
   __shared__ int32_t big_n;
   __shared__ unsigned long long big_base;
+  __shared__ uint32_t excl_lds;
   if (sz->status) return;
   if ((int64_t)blockIdx.x >= nbk) {
     if (rel_ids) relabel_tiles(rel_ids, sz->e[hop - 2], pos_of, blockIdx.x - nbk, gridDim.x - nbk);
     return;
   }
   const int64_t n = sz->n[hop - 1];
-  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   if (threadIdx.x == 0) big_n = 0;
   __syncthreads();
+  int32_t c[kScanItems] = {};
   int32_t s = 0;
-  if (base < n) {
+  if ((int64_t)blockIdx.x * kScanTile < n) {
     int32_t v[kScanItems];
     int64_t lo[kScanItems], hi[kScanItems];
 #pragma unroll
-    for (int it = 0; it < kScanItems; ++it) {
-      const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
-      v[it] = nodes[i < n ? i : n - 1];
-    }
+    for (int it = 0; it < kScanItems; ++it) v[it] = nodes[base + it < n ? base + it : n - 1];
 #pragma unroll
     for (int it = 0; it < kScanItems; ++it) pin(v[it]);
 #pragma unroll
@@ -125,21 +178,33 @@ __global__ __launch_bounds__(kScanNT) void k_row_counts(const int64_t* __restric
     }
 #pragma unroll
     for (int it = 0; it < kScanItems; ++it) {
-      const int64_t i = base + (int64_t)it * kScanNT + threadIdx.x;
+      const int64_t i = base + it;
       if (i < n) {
         const int64_t d = hi[it] - lo[it];
-        const int32_t c = d < fo ? (int32_t)d : fo;
-        bptr[i + 1] = c;
-        s += c;
+        c[it] = d < fo ? (int32_t)d : fo;
+        s += c[it];
         if (d > big_min) big_lds[atomicAdd(&big_n, 1)] = (int32_t)i;
       }
     }
   }
-  s = block_sum<kScanNT>(s, lds);  // (its barriers also complete the big_lds appends)
+  int32_t tot;
+  const int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot);  // (its barriers complete the big_lds appends)
+  const uint32_t before = lookback_exclusive(flags, blockIdx.x, (uint32_t)tot, epoch, &sz->status, &excl_lds);
+  int64_t run = (int64_t)before + ex;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t i = base + it;
+    if (i < n) {
+      run += c[it];
+      bptr[i + 1] = (int32_t)run;
+    }
+  }
   if (threadIdx.x == 0) {
-    partials[blockIdx.x] = s;
-    if (s) atomicAdd((unsigned long long*)&sz->e[hop - 1], (unsigned long long)s);
-    if (blockIdx.x == 0) sz->n[hop] = n;  // new nodes are added by k_bits_count
+    if (blockIdx.x == 0) {
+      bptr[0] = 0;
+      sz->n[hop] = n;  // new nodes are added by k_bits_scan
+    }
+    if ((int64_t)blockIdx.x == nbk - 1) sz->e[hop - 1] = (int64_t)before + tot;
     big_base = big_n ? atomicAdd((unsigned long long*)&sz->n_big[hop - 1], (unsigned long long)big_n) : 0ull;
   }
   __syncthreads();
@@ -174,34 +239,6 @@ __global__ __launch_bounds__(kScanNT) void k_scan_partials(int32_t* __restrict__
   if (threadIdx.x == 0 && total_out) *total_out = (int64_t)carry + (add ? *add : 0);
 }
 
-// bptr[1..n] holds counts; turn bptr[0..n] into exclusive offsets.
-__global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, int hop,
-                                                         int32_t* __restrict__ bptr,
-                                                         const int32_t* __restrict__ partials) {
-  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
-  if (sz->status) return;
-  const int64_t n = sz->n[hop - 1];
-  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  int32_t v[kScanItems];
-  int32_t s = 0;
-#pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    const int64_t i = base + it;
-    v[it] = i < n ? bptr[i + 1] : 0;
-    s += v[it];
-  }
-  const int32_t before = preceding_sum<kScanNT>(partials, blockIdx.x, lds);
-  int32_t tot;
-  int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot) + before;
-#pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    const int64_t i = base + it;
-    ex += v[it];
-    if (i < n) bptr[i + 1] = ex;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) bptr[0] = 0;
-}
-
 // --------------------------------------------------------------- sampler
 // One wavefront per frontier node. Rows with d <= fanout are copied. For
 // longer rows the choice is the fanout positions of smallest (key, j),
@@ -216,7 +253,7 @@ __global__ __launch_bounds__(kScanNT) void k_row_offsets(const StepSizes* sz, in
 //      order (= ascending j), and the chosen positions are written in
 //      ascending j.
 // The chosen ids not yet in the frontier are marked in the new-node bitmap
-// as they are written. Rows longer than big_min (listed by k_row_counts) are
+// as they are written. Rows longer than big_min (listed by k_row_scan) are
 // taken first. Where the frontier is small, so that its few longest rows bound
 // the hop's time, each of them gets a whole block: its waves filter
 // consecutive quarters of the row with the same tau, and the four candidate
@@ -245,7 +282,7 @@ struct SampleArgs {
   uint32_t key0, key1;
   double mu32;              // (fo + 3 sqrt(fo) + 3) * 2^32
   int64_t big_min;          // rows longer than this are listed in big_rows
-  const int32_t* big_rows;  // appended by k_row_counts
+  const int32_t* big_rows;  // appended by k_row_scan
   int64_t row_waves;        // k_sample_waves: waves [0, row_waves) take the big list, the rest all rows
   int64_t big_blocks;       // k_sample_blocks: blocks [0, big_blocks) walk the big list, one row per
                             // block; the rest take all other rows, one per wave
@@ -601,48 +638,26 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_blocks(SampleA
 }
 
 // ------------------------------------------------------------ dedup/relabel
-// Per-block popcount of the bitmap tile.
-__global__ __launch_bounds__(kScanNT) void k_bits_count(const uint32_t* __restrict__ bits, int64_t W,
-                                                        StepSizes* sz, int hop,
-                                                        int32_t* __restrict__ partials) {
-  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
-  if (sz->status) return;
-  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  int32_t s = 0;
-  if (base + kScanItems <= W) {
-    const uint4 w4 = *reinterpret_cast<const uint4*>(bits + base);
-    s = __popc(w4.x) + __popc(w4.y) + __popc(w4.z) + __popc(w4.w);
-  } else {
-    for (int it = 0; it < kScanItems; ++it)
-      if (base + it < W) s += __popc(bits[base + it]);
-  }
-  s = block_sum<kScanNT>(s, lds);
-  if (threadIdx.x == 0) {
-    partials[blockIdx.x] = s;
-    if (s) atomicAdd((unsigned long long*)&sz->n[hop], (unsigned long long)s);
-  }
-}
-
 // New nodes in ascending id: F[n_{k-1} + rank] = u, pos_of[u] = that
-// position; the bitmap is cleared for the next hop.
-__global__ __launch_bounds__(kScanNT) void k_bits_emit(uint32_t* __restrict__ bits, int64_t W,
-                                                       const StepSizes* sz, int hop,
-                                                       const int32_t* __restrict__ partials,
-                                                       int32_t* __restrict__ nodes,
-                                                       int32_t* __restrict__ pos_of) {
+// position, with the rank from the single-pass scan of the bitmap's
+// popcounts; the bitmap is cleared for the next hop. The last tile writes
+// n_k. (bits holds W + 4 words, the last four always zero.)
+__global__ __launch_bounds__(kScanNT) void k_bits_scan(uint32_t* __restrict__ bits, int64_t W, StepSizes* sz,
+                                                       int hop, uint64_t* flags, uint32_t epoch,
+                                                       int32_t* __restrict__ nodes, int32_t* __restrict__ pos_of) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  __shared__ uint32_t excl_lds;
   if (sz->status) return;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  uint32_t w[kScanItems];
-  int32_t s = 0;
-#pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    w[it] = base + it < W ? bits[base + it] : 0u;
-    s += __popc(w[it]);
-  }
-  const int32_t before = preceding_sum<kScanNT>(partials, blockIdx.x, lds);
+  uint4 w4 = make_uint4(0u, 0u, 0u, 0u);
+  if (base < W) w4 = *reinterpret_cast<const uint4*>(bits + base);
+  const uint32_t w[kScanItems] = {w4.x, w4.y, w4.z, w4.w};
+  const int32_t s = __popc(w[0]) + __popc(w[1]) + __popc(w[2]) + __popc(w[3]);
   int32_t tot;
-  int64_t off = (int64_t)block_exclusive_scan<kScanNT>(s, lds, &tot) + before + sz->n[hop - 1];
+  const int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot);
+  const uint32_t before = lookback_exclusive(flags, blockIdx.x, (uint32_t)tot, epoch, &sz->status, &excl_lds);
+  const int64_t n_prev = sz->n[hop - 1];
+  int64_t off = n_prev + before + ex;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
     uint32_t x = w[it];
@@ -658,10 +673,11 @@ __global__ __launch_bounds__(kScanNT) void k_bits_emit(uint32_t* __restrict__ bi
     }
     bits[base + it] = 0u;
   }
+  if (threadIdx.x == 0 && blockIdx.x == gridDim.x - 1) sz->n[hop] = n_prev + before + tot;
 }
 
 // Relabel the last hop's sampled ids to their frontier positions (earlier
-// hops are relabelled by the next hop's k_row_counts).
+// hops are relabelled by the next hop's k_row_scan).
 __global__ __launch_bounds__(kScanNT) void k_relabel(int32_t* __restrict__ ids, const StepSizes* sz, int hop,
                                                      const int32_t* __restrict__ pos_of) {
   if (sz->status) return;
