@@ -85,6 +85,15 @@ __device__ __forceinline__ T block_sum(T v, T* lds) {
   return total;
 }
 
+// a ^ b ^ key in one instruction: gfx950's three-input bitwise operation
+// (truth table 0x96 = XOR of all three); key is wave-uniform (an SGPR, the
+// one scalar operand the instruction may take).
+__device__ __forceinline__ uint32_t xor3_key(uint32_t a, uint32_t b, uint32_t key) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(key));
+  return r;
+}
+
 // Philox4x32-10 block function (Salmon, Moraes, Dror, Shaw, SC'11): ten
 // rounds; each round takes the 64-bit products of counter words 0 and 2
 // with two fixed multipliers, mixes their high halves with words 1 and 3

@@ -321,7 +321,8 @@ struct PhiloxRow {
       r1 += 0xBB67AE85u;
       const uint64_t a = (uint64_t)0xD2511F53u * c.x;
       const uint64_t b = (uint64_t)0xCD9E8D57u * c.z;
-      c = make_uint4((uint32_t)(b >> 32) ^ c.y ^ r0, (uint32_t)b, (uint32_t)(a >> 32) ^ c.w ^ r1, (uint32_t)a);
+      c = make_uint4(xor3_key((uint32_t)(b >> 32), c.y, r0), (uint32_t)b, xor3_key((uint32_t)(a >> 32), c.w, r1),
+                     (uint32_t)a);
     }
     return c;
   }
