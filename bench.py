@@ -70,10 +70,13 @@ def build_inputs(w, threads=None):
     return g, local, store, sched
 
 
-def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False, depth=None):
+def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False, depth=None,
+                timed_groups=("gather_hbm",), prof_steps=64):
     """One context over steps 0..warmup+steps-1 with look-ahead (`depth`
-    batches in flight); the last `steps` are timed. Returns the raw
-    measurements."""
+    batches in flight); the last `steps` are timed, with HIP events only on
+    `timed_groups` (every timed group adds event packets to the streams).
+    Then `prof_steps` further steps with every group timed give the phase
+    breakdown. Returns the raw measurements."""
     import torch
     from paper_2410_22697_amd import Massive
     depth = depth or DEFAULT_DEPTH
@@ -86,7 +89,8 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     log("massive_init %.2fs: cap=%d alpha=%.6g" % (init_s, gm.cap, gm.alpha))
     bbs = [gm.alloc_batch(w.batch) for _ in range(depth)]
     total = warmup + steps
-    seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
+    seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda()
+                 for t in range(total + prof_steps)]
     torch.cuda.synchronize()
 
     if copy_probe:
@@ -133,7 +137,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     log("warmup %d steps done" % warmup)
     r0, e0 = gm.counters()
     f0 = gm.refilled_rows()
-    gm.set_timing(True)
+    gm.set_timing(timed_groups)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     run(warmup, total)
@@ -142,10 +146,19 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     tim = gm.timing()
     r1, e1 = gm.counters()
     f1 = gm.refilled_rows()
+    tim_prof, stats_prof = None, None
+    if prof_steps:
+        n_timed = len(stats)
+        gm.set_timing(True)
+        run(total, total + prof_steps)
+        tim_prof = gm.timing()
+        stats_prof = np.array(stats[n_timed:], np.float64)
+        del stats[n_timed:], sizes[n_timed:]
     out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
                depth=depth,
                stats=np.array(stats, np.float64), sizes=sizes, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
-               refilled=f1 - f0, first_steps=first_steps)
+               refilled=f1 - f0, first_steps=first_steps, tim_prof=tim_prof, stats_prof=stats_prof,
+               prof_steps=prof_steps)
     del bbs, seeds_dev
     gm.close()
     return out
@@ -206,8 +219,13 @@ def summarize(w, res):
     g_ms, g_calls = tim["gather_hbm"]
     g_bytes = float(np.mean(2 * hbm_rows * rb + 8 * hbm_rows))
     g_avg_s = g_ms / 1e3 / max(g_calls, 1)
-    m_ms, m_calls = tim["gather_miss"]
-    m_bytes = float(np.mean(host_rows * rb))
+    # the miss gather's own rate: from the steps with every group timed, if any
+    if res.get("tim_prof"):
+        m_ms, m_calls = res["tim_prof"]["gather_miss"]
+        m_bytes = float(np.mean(res["stats_prof"][:, 4] * rb))
+    else:
+        m_ms, m_calls = tim["gather_miss"]
+        m_bytes = float(np.mean(host_rows * rb))
     refill_bytes = res["refilled"] * rb / max(K, 1)  # copied by refill chunks inside the timed region, per step
     sz = res["sizes"][res["warmup"]:]
     b_alg = float(np.mean([alg_hbm_bytes(n, e, l, h, m, rb) for (n, e), (l, h, m) in zip(sz, st[:, :3])]))
@@ -285,7 +303,9 @@ def main():
         "%.1f MB refill copied (%.1f MB evicted); %.1f GB/s over the link" %
         (sm["m_bytes"] / 1e6, sm["pend_bytes"] / 1e6, sm["refill_bytes"] / 1e6, sm["evicted_bytes"] / 1e6,
          sm["link_gbps"]))
-    for name, (ms, calls) in res["tim"].items():
+    phases, P = (res["tim_prof"], res["prof_steps"]) if res.get("tim_prof") else (res["tim"], K)
+    log("HIP-event timing: gather_hbm over the timed steps; every group over %d further steps:" % P)
+    for name, (ms, calls) in phases.items():
         log("  %-13s %9.3f ms total, %5d launches, %.1f us avg" % (name, ms, calls, 1e3 * ms / max(calls, 1)))
     log("gather_hbm %.0f B/launch, %.1f us, %.1f GB/s (%.1f%% of HBM); miss fetch %.1f GB/s; hit rate %.3f" %
         (sm["g_bytes"], sm["g_avg_s"] * 1e6, sm["g_gbps"], 100 * sm["g_gbps"] / HBM_PEAK_GBPS, sm["m_gbps"],
@@ -341,7 +361,8 @@ def main():
                                "link_GBps": round(sm["mbps"] * sm["link_bytes"] / 1e9, 2),
                                "link_peak_GBps": PCIE_PEAK_GBPS,
                                "link_frac": round(sm["mbps"] * sm["link_bytes"] / 1e9 / PCIE_PEAK_GBPS, 4)},
-        "phase_ms_per_step": {k: round(v[0] / K, 4) for k, v in res["tim"].items()},
+        "phase_ms_per_step": {k: round(v[0] / P, 4) for k, v in phases.items()},
+        "phases_from": "%d steps after the timed region, every kernel group timed with HIP events" % P,
         "init_s": round(res["init_s"], 3),
         "cpu_baseline": cpu,
     }
@@ -396,7 +417,7 @@ def sweep(w, g, local, store, sched, args):
     total = warm + steps
 
     def point(kind, wm, base):
-        res = run_context(wm, g, local, store, sched, warm, steps)
+        res = run_context(wm, g, local, store, sched, warm, steps, timed_groups=True, prof_steps=0)
         sm = summarize(wm, res)
         st = res["stats"]
         hr = st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)

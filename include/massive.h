@@ -178,8 +178,13 @@ int massive_get_buffer_rows(massive_ctx* ctx, void* host_out);
 int massive_info(const massive_ctx* ctx, int64_t* cap, float* alpha);
 
 /* Per-kernel-group timing with HIP events recorded on the stream each group
- * runs on. enable != 0 turns it on (and clears the totals). */
-int massive_set_timing(massive_ctx* ctx, int enable);
+ * runs on (the groups of massive_get_timing). groups is a bit mask, bit i for
+ * group i (MASSIVE_TIMING_ALL: every group, 0: off); it clears the totals.
+ * Each timed group adds event packets to its streams, so a run that must not
+ * be slowed times only what it needs. MASSIVE_EINVAL for bits outside the
+ * mask. */
+#define MASSIVE_TIMING_ALL 0x3F
+int massive_set_timing(massive_ctx* ctx, int groups);
 /* Totals since enabled: out_ms[i] summed milliseconds and out_calls[i]
  * launches for i = 0 sample+dedup, 1 classify, 2 gather_hbm, 3 gather_miss,
  * 4 eviction round, 5 refill. Synchronises the context's streams. */

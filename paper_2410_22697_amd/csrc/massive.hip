@@ -136,7 +136,7 @@ struct massive_ctx {
     int32_t n0 = 0;
   } infl[kSlots];
   // timing
-  bool timing = false;
+  int timing = 0;  // bit g: group g is timed
   std::vector<hipEvent_t> ev_pool;
   std::vector<TimedRange> pending;
   double tms[6] = {};
@@ -169,7 +169,7 @@ struct massive_ctx {
     int group;
     hipEvent_t a = nullptr;
     Range(massive_ctx* c_, hipStream_t s_, int g) : c(c_), s(s_), group(g) {
-      if (c->timing && (a = c->ev_get())) (void)hipEventRecord(a, s);
+      if (((c->timing >> g) & 1) && (a = c->ev_get())) (void)hipEventRecord(a, s);
     }
     ~Range() {
       if (!a) return;
@@ -180,9 +180,9 @@ struct massive_ctx {
     }
   };
   // a start/stop pair that hipExtLaunchKernelGGL stamps around one dispatch
-  bool kernel_pair(hipEvent_t* a, hipEvent_t* b) {
+  bool kernel_pair(int group, hipEvent_t* a, hipEvent_t* b) {
     *a = *b = nullptr;
-    if (!timing) return false;
+    if (!((timing >> group) & 1)) return false;
     *a = ev_get();
     *b = ev_get();
     if (!*a || !*b) return false;
@@ -267,7 +267,7 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
                    const int64_t* count, const uint8_t* src, uint8_t* dst, int64_t rb, int64_t max_rows,
                    int64_t max_blocks, const int32_t* wslot = nullptr, uint8_t* buf = nullptr) {
   hipEvent_t ea = nullptr, eb = nullptr;
-  const bool timed = c->kernel_pair(&ea, &eb);
+  const bool timed = c->kernel_pair(group, &ea, &eb);
   int vec = 4;
   const uintptr_t al = (uintptr_t)src | (uintptr_t)dst | (uintptr_t)buf;
   if (rb % 16 == 0 && al % 16 == 0)
@@ -318,7 +318,7 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
 void launch_refill(massive_ctx* c, hipStream_t s, const int64_t* count, int64_t max_rows, int32_t round_id,
                    int32_t chunk, int32_t nchunks) {
   hipEvent_t ea = nullptr, eb = nullptr;
-  const bool timed = c->kernel_pair(&ea, &eb);
+  const bool timed = c->kernel_pair(5, &ea, &eb);
   const uint8_t* src = c->d_store;
   uint8_t* dst = c->d_slab;
   const int64_t rb = c->rb;
@@ -1013,11 +1013,13 @@ int massive_info(const massive_ctx* c, int64_t* cap, float* alpha) {
   return MASSIVE_OK;
 }
 
-int massive_set_timing(massive_ctx* c, int enable) {
+int massive_set_timing(massive_ctx* c, int groups) {
   if (!c) return MASSIVE_EINVAL;
+  if (groups & ~MASSIVE_TIMING_ALL) return c->fail(MASSIVE_EINVAL, "timing groups 0x%x outside 0x%x", groups,
+                                                   MASSIVE_TIMING_ALL);
   CK(hipDeviceSynchronize());
   c->resolve_timing();
-  c->timing = enable != 0;
+  c->timing = groups;
   for (int i = 0; i < 6; ++i) {
     c->tms[i] = 0.0;
     c->tcalls[i] = 0;

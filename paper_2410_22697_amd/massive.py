@@ -97,6 +97,7 @@ def _ptr(x) -> Optional[int]:
 
 
 TIMING_GROUPS = ("sample_dedup", "classify", "gather_hbm", "gather_miss", "evict_round", "refill")
+TIMING_ALL = 0x3F
 
 
 @dataclass
@@ -280,8 +281,16 @@ class Massive:
         self._check(self._lib.massive_get_buffer_rows(self._h, out.ctypes.data))
         return out[:self.cap]
 
-    def set_timing(self, on: bool):
-        self._check(self._lib.massive_set_timing(self._h, 1 if on else 0))
+    def set_timing(self, on=True):
+        """on: True (every group), False (off), or an iterable of group names
+        from TIMING_GROUPS."""
+        if on is True or on is False:
+            mask = TIMING_ALL if on else 0
+        else:
+            mask = 0
+            for g in on:
+                mask |= 1 << TIMING_GROUPS.index(g)
+        self._check(self._lib.massive_set_timing(self._h, mask))
 
     def timing(self):
         ms = np.zeros(6, np.float64)

@@ -25,9 +25,10 @@ def test_header_declares_the_three_calls():
 def test_binding_constants_match_the_header():
     from paper_2410_22697_amd import massive
     text = open(HEADER).read()
-    defs = dict(re.findall(r"#define (MASSIVE_[A-Z_]+) \(?(-?\d+)\)?", text))
+    defs = dict(re.findall(r"#define (MASSIVE_[A-Z_]+) \(?(-?(?:0x[0-9A-Fa-f]+|\d+))\)?", text))
     assert int(defs["MASSIVE_MAX_HOPS"]) == massive.MAX_HOPS
     assert int(defs["MASSIVE_MAX_INFLIGHT"]) == massive.MAX_INFLIGHT
+    assert int(defs["MASSIVE_TIMING_ALL"], 0) == massive.TIMING_ALL == (1 << len(massive.TIMING_GROUPS)) - 1
     for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE"):
         assert int(defs["MASSIVE_" + name]) == getattr(massive, name), name
 
