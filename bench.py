@@ -237,6 +237,7 @@ def summarize(w, res):
                 m_gbps=m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9 if m_ms > 0 else 0.0,
                 hit_rate=float(hit.sum() / max(hit.sum() + mis.sum(), 1)),
                 pend_bytes=float(np.mean((host_rows - mis) * rb)), refill_bytes=refill_bytes,
+                host_bytes=float(np.mean(host_rows * rb)),
                 evicted_bytes=res["evicted"] * rb / max(K, 1),
                 link_gbps=(float(host_rows.sum()) * rb + res["refilled"] * rb) / res["elapsed"] / 1e9,
                 remote_rows=float(np.mean(host_rows)) + res["refilled"] / max(K, 1),
@@ -301,7 +302,7 @@ def main():
         (K, res["elapsed"], sm["mbps"], res["rounds"], res["evicted"]))
     log("host link per step: %.1f MB miss gather (%.1f MB of them hits on refilling slots, written through), "
         "%.1f MB refill copied (%.1f MB evicted); %.1f GB/s over the link" %
-        (sm["m_bytes"] / 1e6, sm["pend_bytes"] / 1e6, sm["refill_bytes"] / 1e6, sm["evicted_bytes"] / 1e6,
+        (sm["host_bytes"] / 1e6, sm["pend_bytes"] / 1e6, sm["refill_bytes"] / 1e6, sm["evicted_bytes"] / 1e6,
          sm["link_gbps"]))
     phases, P = (res["tim_prof"], res["prof_steps"]) if res.get("tim_prof") else (res["tim"], K)
     log("HIP-event timing: gather_hbm over the timed steps; every group over %d further steps:" % P)
