@@ -135,3 +135,28 @@ def test_long_rows_by_blocks(monkeypatch, big_row, big_blocks):
     assert rounds == 2
     prob, sched, w = workload_problem("cl10k", fanout=(200, 30), delta=3)
     run_parity("cl10k fanout 200 big rows > %d" % big_row, prob, sched.seeds, 6)
+
+
+def test_timing_groups():
+    # only the selected kernel groups carry HIP events; a mask outside the
+    # groups is refused
+    from paper_2410_22697_amd import MassiveError, TIMING_GROUPS
+    prob, sched, w = workload_problem("cl10k", delta=2)
+    gm = make_gpu(prob)
+    bb = gm.alloc_batch(w.batch)
+    gm.set_timing(["gather_hbm", "classify"])
+    for t in range(3):
+        gm.sample(to_dev(sched.seeds(t)), bb)
+        gm.evict_step()
+    tim = gm.timing()
+    assert set(tim) == set(TIMING_GROUPS)
+    assert tim["gather_hbm"][1] == 3 and tim["classify"][1] == 3 and tim["gather_hbm"][0] > 0
+    assert all(tim[g][1] == 0 for g in TIMING_GROUPS if g not in ("gather_hbm", "classify"))
+    gm.set_timing(True)
+    gm.sample(to_dev(sched.seeds(3)), bb)
+    gm.evict_step()
+    tim = gm.timing()
+    assert tim["sample_dedup"][1] == 1 and tim["gather_hbm"][1] == 1 and tim["gather_miss"][1] == 1
+    with pytest.raises(MassiveError) as ei:
+        gm._check(gm._lib.massive_set_timing(gm._h, 1 << len(TIMING_GROUPS)))
+    assert ei.value.code == -1
