@@ -141,7 +141,12 @@ int massive_sample(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, mass
  * context then refuses further work with MASSIVE_ESTATE). */
 int massive_sample_async(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
 
-/* Waits for the batch enqueued with io and writes its sizes and counters. */
+/* Waits for the batch enqueued with io and writes its sizes and counters.
+ * MASSIVE_EINVAL for a seed out of [0, L) or repeated (the step is taken
+ * back if no later step was issued); MASSIVE_EHIP, and the context refuses
+ * further work, if the sampler's threshold search found no acceptable
+ * candidate count or a single-pass scan waited past its bound (neither is
+ * expected), or if an eviction round produced inconsistent indices. */
 int massive_batch_wait(massive_ctx* ctx, massive_batch* io);
 
 /* The eviction round owed by the step just sampled; must be called once after
@@ -174,7 +179,7 @@ int massive_get_state(massive_ctx* ctx, int32_t* slot_id, float* S_E, float* S_A
 /* Host copy of the HBM buffer's rows, [cap * row_bytes]. */
 int massive_get_buffer_rows(massive_ctx* ctx, void* host_out);
 
-/* cap (buffer slots), alpha, and the library's internal HIP streams. */
+/* cap (buffer slots) and alpha (each pointer may be NULL). */
 int massive_info(const massive_ctx* ctx, int64_t* cap, float* alpha);
 
 /* Per-kernel-group timing with HIP events recorded on the stream each group
