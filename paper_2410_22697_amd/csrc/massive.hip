@@ -1,9 +1,11 @@
 // massive.hip - libmassive: the C ABI of include/massive.h on one MI355X.
 //
-// Streams: every step runs on the caller's stream ("main"); misses are
-// gathered from pinned host memory on a side stream concurrently with the
-// HBM gather; the refill copy of an eviction round runs on a copy stream and
-// overlaps the next step's sampling (the next HBM gather waits for it).
+// Streams: a step's sampling and classify run on the caller's stream
+// ("main"); its HBM gather, its miss gather from pinned host memory and its
+// completion kernel follow on a side stream, so the main stream goes on to the
+// next step at once; eviction rounds and their refill copies run on a copy
+// stream (the refill chunks and the HBM gathers wait for each other, and the
+// next classify waits for a round).
 // All device memory is allocated in massive_init; the per-step calls do not
 // allocate.
 #include <hip/hip_ext.h>
@@ -97,7 +99,7 @@ struct massive_ctx {
   ms::StepSizes* d_sz = nullptr;      // [kSlots], by step slot
   ms::StepSizes* h_sz = nullptr;      // [kSlots] pinned mailboxes
   int32_t* h_bad = nullptr;           // [kSlots] pinned: eviction-round consistency flag
-  ms::StepSizes* hd_sz = nullptr;     // device views of the two mailboxes
+  ms::StepSizes* hd_sz = nullptr;     // device views of the mailboxes
   int32_t* hd_bad = nullptr;
   ms::RoundState* d_rs = nullptr;
   ms::RoundState* h_rs = nullptr;     // pinned mailbox
