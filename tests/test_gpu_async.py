@@ -83,6 +83,15 @@ def test_lookahead_cl2m45_inflight_refills():
     assert rounds == 2 and pending > 0  # hits on refilling slots were written through
 
 
+@pytest.mark.parametrize("depth", [2, 3])
+def test_lookahead_round_every_step(depth):
+    # delta 1: a round after every step, each refill in one chunk that the
+    # next round must flush first, with two or three batches in flight
+    prob, sched, w = workload_problem("cl10k", delta=1, gamma=0.9)
+    rounds, pending = run_lookahead("async cl10k delta 1 depth %d" % depth, prob, sched.seeds, 12, depth)
+    assert rounds >= 8
+
+
 def test_lookahead_rejects_one_batch_too_many():
     from paper_2410_22697_amd import MAX_INFLIGHT, MassiveError
     prob, sched, w = workload_problem("cl10k")

@@ -38,7 +38,8 @@ def test_cl10k_full_run():
                                   dict(buffer_pct=100, delta=2),                # no candidates at all
                                   dict(buffer_pct=0, delta=2),                  # empty buffer
                                   dict(gamma=1.0, delta=2),                     # nothing ever decays below alpha
-                                  dict(fanout=(40, 30, 2), delta=5)])           # rows up to 320 long, long-row path
+                                  dict(fanout=(40, 30, 2), delta=5),            # rows up to 320 long, long-row path
+                                  dict(gamma=0.9, delta=1)])                    # a round after every step
 def test_cl10k_variants(over):
     prob, sched, w = workload_problem("cl10k", **over)
     run_parity("cl10k%s" % sorted(over.items()), prob, sched.seeds, 20, buffer_rows_every=4)
