@@ -435,10 +435,18 @@ __device__ __forceinline__ int filter_groups(const PhiloxRow& ph, uint32_t g0, u
     // masks: the usual iteration of a long row takes none)
     uint64_t m0, m1, m2, m3;
     if (q0 + MS_WAVE <= g1 && 4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
-      m0 = ballot(wv.x <= tm1);
-      m1 = ballot(wv.y <= tm1);
-      m2 = ballot(wv.z <= tm1);
-      m3 = ballot(wv.w <= tm1);
+      // one test on the smallest of the four keys first (the usual case:
+      // none below tau); the keys are pinned so the four tests stay behind it
+      if (!ballot(min(min(wv.x, wv.y), min(wv.z, wv.w)) <= tm1)) continue;
+      uint4 k4 = wv;
+      pin(k4.x);
+      pin(k4.y);
+      pin(k4.z);
+      pin(k4.w);
+      m0 = ballot(k4.x <= tm1);
+      m1 = ballot(k4.y <= tm1);
+      m2 = ballot(k4.z <= tm1);
+      m3 = ballot(k4.w <= tm1);
     } else {
       const bool in = q < g1;
       m0 = ballot(in && 4 * q < d32 && wv.x <= tm1);
@@ -506,10 +514,9 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_waves(SampleAr
       // masks: the usual iteration of a long row takes none)
       uint64_t m0, m1, m2, m3;
       if (4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
-        // one test on the smallest of the four keys: the usual iteration
-        // has no key below tau
+        // one test on the smallest of the four keys first (the usual case:
+        // none below tau); the keys are pinned so the four tests stay behind it
         if (!ballot(min(min(wv.x, wv.y), min(wv.z, wv.w)) <= tm1)) continue;
-        // (the keys pinned here, so the four tests stay on this rare path)
         uint4 k4 = wv;
         pin(k4.x);
         pin(k4.y);
