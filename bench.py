@@ -270,7 +270,12 @@ def main():
     ap.add_argument("--compare", action="store_true",
                     help="the paper's comparison on the same inputs: no buffer (f = 0), prefetch without "
                          "eviction (no round within the run) and prefetch with eviction; one JSON line each")
+    ap.add_argument("--compare-mode", choices=COMPARE_MODES, default=None,
+                    help="run one mode of --compare in this process (used by --compare itself)")
     args = ap.parse_args()
+    if args.compare and args.compare_mode is None:
+        compare([a for a in sys.argv[1:]])
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each partition's "
               "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
@@ -285,7 +290,7 @@ def main():
         w = w.with_(**over)
     g, local, store, sched = build_inputs(w, args.threads)
     if args.compare:
-        compare(w, g, local, store, sched, args)
+        print(json.dumps(compare_one(w, args.compare_mode, g, local, store, sched, args)), flush=True)
         return
     if args.sweep:
         sweep(w, g, local, store, sched, args)
@@ -370,43 +375,67 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def compare(w, g, local, store, sched, args):
+COMPARE_MODES = ("no_buffer", "static", "eviction")
+
+
+def compare_workload(w, name, total):
+    """The workload of one --compare mode."""
+    if name == "no_buffer":
+        return w.with_(buffer_pct=0)
+    if name == "static":
+        return w.with_(delta=total + 1)  # no round within the run
+    return w
+
+
+def compare_one(w, name, g, local, store, sched, args):
+    """One mode of the paper's comparison (Section V) in this process: the
+    measurements of the JSON line, without the ratios to the no-buffer mode."""
+    wm = compare_workload(w, name, args.warmup + args.steps)
+    log("mode %s: f=%d%% delta=%d gamma=%g" % (name, wm.buffer_pct, wm.delta, wm.gamma))
+    res = run_context(wm, g, local, store, sched, args.warmup, args.steps)
+    sm = summarize(wm, res)
+    st = res["stats"]
+    series = (st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)).round(4).tolist()  # per step, from step 0
+    return {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": name,
+            "value": round(sm["mbps"], 3), "unit": "minibatches/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "dtype": "f32" if wm.dtype == "f32" else "bf16",
+            "config": {"workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
+                       "cap": res["gm_cap"], "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"]},
+            "init_s": round(res["init_s"], 3), "init_rows_over_link": res["gm_cap"],
+            "hit_rate": round(sm["hit_rate"], 4),
+            "halo_rows_per_step": round(sm["halo_rows"], 1),
+            "remote_rows_per_step": round(sm["remote_rows"], 1),
+            "miss_gather_rows_per_step": round(sm["host_bytes"] / wm.row_bytes, 1),
+            "refill_rows_per_step": round(sm["refill_bytes"] / wm.row_bytes, 1),
+            "link_GBps_whole_run": round(sm["link_gbps"], 2),
+            "gather_frac_hbm": round(sm["g_gbps"] / HBM_PEAK_GBPS, 4),
+            "hit_rate_per_step": series}
+
+
+def compare(argv):
     """The paper's comparison (Section V) on one partition's share: no buffer
     (every halo row over the link, the baseline without prefetching), prefetch
     without eviction (the initial degree-ranked buffer kept for the whole run)
     and prefetch with eviction. Same graph, features and seed schedule; each
-    mode from a fresh context, over the same steps."""
-    total = args.warmup + args.steps
-    modes = [("no_buffer", w.with_(buffer_pct=0)),
-             ("static", w.with_(delta=total + 1)),   # no round within the run
-             ("eviction", w)]
-    base = None
-    for name, wm in modes:
-        log("mode %s: f=%d%% delta=%d gamma=%g" % (name, wm.buffer_pct, wm.delta, wm.gamma))
-        res = run_context(wm, g, local, store, sched, args.warmup, args.steps)
-        sm = summarize(wm, res)
-        if base is None:
-            base = sm
-        st = res["stats"]
-        series = (st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)).round(4).tolist()  # per step, from step 0
-        out = {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": name,
-               "value": round(sm["mbps"], 3), "unit": "minibatches/s", "n_gpus": 1, "steps": args.steps,
-               "warmup": args.warmup, "dtype": "f32" if wm.dtype == "f32" else "bf16",
-               "config": {"workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
-                          "cap": res["gm_cap"], "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"]},
-               "init_s": round(res["init_s"], 3), "init_rows_over_link": res["gm_cap"],
-               "hit_rate": round(sm["hit_rate"], 4),
-               "halo_rows_per_step": round(sm["halo_rows"], 1),
-               "remote_rows_per_step": round(sm["remote_rows"], 1),
-               "remote_rows_vs_no_buffer": round(sm["remote_rows"] / max(base["remote_rows"], 1e-9), 4),
-               "miss_gather_rows_per_step": round(sm["m_bytes"] / wm.row_bytes, 1),
-               "refill_rows_per_step": round(sm["refill_bytes"] / wm.row_bytes, 1),
-               "link_GBps_whole_run": round(sm["link_gbps"], 2),
-               "speedup_vs_no_buffer": round(sm["mbps"] / base["mbps"], 4),
-               "gather_frac_hbm": round(sm["g_gbps"] / HBM_PEAK_GBPS, 4),
-               "hit_rate_per_step": series}
+    mode in a process of its own, started from this one (which does not use
+    the GPU): a context created after others in one process was measured up to
+    29% slower, whatever its mode."""
+    import subprocess
+    outs = {}
+    for name in COMPARE_MODES:
+        cmd = [sys.executable, os.path.abspath(__file__)] + argv + ["--compare-mode", name]
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            log("mode %s failed with status %d" % (name, r.returncode))
+            sys.exit(r.returncode)
+        outs[name] = json.loads([l for l in r.stdout.splitlines() if l.startswith("{")][-1])
+    base = outs["no_buffer"]
+    for name in COMPARE_MODES:
+        out = outs[name]
+        out["remote_rows_vs_no_buffer"] = round(out["remote_rows_per_step"] / max(base["remote_rows_per_step"], 1e-9), 4)
+        out["speedup_vs_no_buffer"] = round(out["value"] / base["value"], 4)
         log("mode %s: %.1f minibatches/s, hit rate %.3f, %.0f remote rows per step (%.3f of no buffer)" %
-            (name, sm["mbps"], sm["hit_rate"], sm["remote_rows"], out["remote_rows_vs_no_buffer"]))
+            (name, out["value"], out["hit_rate"], out["remote_rows_per_step"], out["remote_rows_vs_no_buffer"]))
         print(json.dumps(out), flush=True)
 
 
