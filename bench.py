@@ -418,8 +418,8 @@ def compare(argv):
     without eviction (the initial degree-ranked buffer kept for the whole run)
     and prefetch with eviction. Same graph, features and seed schedule; each
     mode in a process of its own, started from this one (which does not use
-    the GPU): a context created after others in one process was measured up to
-    29% slower, whatever its mode."""
+    the GPU): with the three modes in one process, the third context was
+    measured 8-29% slower, whichever mode it was."""
     import subprocess
     outs = {}
     for name in COMPARE_MODES:
