@@ -92,6 +92,28 @@ def test_lookahead_round_every_step(depth):
     assert rounds >= 8
 
 
+def test_invalid_seeds_with_later_steps_in_flight():
+    # a step whose seeds are invalid cannot be taken back once a later step
+    # was issued: its wait reports the seeds and the context refuses further
+    # work; the batches around it complete normally (no kernel waits on it)
+    from paper_2410_22697_amd import MassiveError
+    prob, sched, w = workload_problem("cl10k")
+    gm = make_gpu(prob)
+    bbs = [gm.alloc_batch(w.batch) for _ in range(3)]
+    seeds = [to_dev(sched.seeds(0)), to_dev(np.array([3, 3], np.int32)), to_dev(sched.seeds(2))]
+    for t in range(3):
+        gm.sample_async(seeds[t], bbs[t])
+        gm.evict_step(wait=False)
+    gm.wait(bbs[0])
+    with pytest.raises(MassiveError) as ei:
+        gm.wait(bbs[1])
+    assert ei.value.code == -1
+    gm.wait(bbs[2])
+    with pytest.raises(MassiveError) as ei:
+        gm.sample_async(seeds[0], bbs[0])
+    assert ei.value.code == -5
+
+
 def test_lookahead_rejects_one_batch_too_many():
     from paper_2410_22697_amd import MAX_INFLIGHT, MassiveError
     prob, sched, w = workload_problem("cl10k")
