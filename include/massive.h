@@ -77,7 +77,7 @@ typedef struct {
   const void* halo_store;     /* PINNED host [H * row_bytes] (hipHostMalloc'd,
                                  e.g. a torch pin_memory tensor): the remote
                                  features; read by the GPU over the host link */
-  int64_t row_bytes;          /* bytes per feature row, multiple of 4         */
+  int64_t row_bytes;          /* bytes per feature row, multiple of 4, <= 1 MiB */
   int32_t K;                  /* hops, 1..MASSIVE_MAX_HOPS                     */
   int32_t fanout[MASSIVE_MAX_HOPS]; /* hop-first fanouts, each >= 1           */
   int32_t buffer_pct;         /* f_p^h as an integer percent, 0..100          */

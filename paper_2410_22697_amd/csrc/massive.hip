@@ -598,7 +598,11 @@ int massive_init(const massive_init_args* a, massive_ctx** out) {
   if (!a->indptr || !a->indices) return bad("indptr / indices are NULL");
   if (a->L > 0 && !a->local_feat) return bad("local_feat is NULL");
   if (a->H > 0 && (!a->halo_store || !a->halo_gid || !a->halo_degree)) return bad("halo arrays are NULL");
-  if (a->row_bytes <= 0 || a->row_bytes % 4) return bad("row_bytes must be a positive multiple of 4");
+  // (at most 1 MiB keeps the copy kernels' division by chunks per row, a
+  // multiply by a rounded-up reciprocal, exact for every chunk index that fits
+  // in device memory)
+  if (a->row_bytes <= 0 || a->row_bytes % 4 || a->row_bytes > (1 << 20))
+    return bad("row_bytes must be a positive multiple of 4, at most 1 MiB");
   if (a->K < 1 || a->K > MASSIVE_MAX_HOPS) return bad("K must be in 1..8");
   for (int k = 0; k < a->K; ++k)
     if (a->fanout[k] < 1 || a->fanout[k] > 256) return bad("every fanout must be in 1..256");

@@ -61,7 +61,8 @@ def test_init_error_path_without_gpu():
 _BAD = [("K", 0, b"K must"), ("K", 9, b"K must"), ("fanout0", 0, b"fanout"), ("fanout0", 257, b"fanout"),
         ("buffer_pct", 101, b"buffer_pct"), ("buffer_pct", -1, b"buffer_pct"), ("gamma", 0.0, b"gamma"),
         ("gamma", 1.5, b"gamma"), ("delta", 0, b"delta"), ("row_bytes", 6, b"row_bytes"),
-        ("row_bytes", 0, b"row_bytes"), ("L", -1, b"L >= 0")]
+        ("row_bytes", 0, b"row_bytes"), ("row_bytes", (1 << 20) + 4, b"row_bytes"),
+        ("L", -1, b"L >= 0")]
 
 
 @pytest.mark.parametrize("field,value,msg", _BAD)

@@ -1,0 +1,32 @@
+"""The copy kernels flatten (row, 16/8/4-byte chunk) work and recover the row
+of chunk index n as n * magic >> 64 with magic = floor((2^64 - 1) / cpr) + 1,
+cpr the chunks per row. This checks, with exact integers, that the quotient
+is n // cpr for every cpr a row of at most 1 MiB can have, at the chunk
+indices where an error would show first (just below and at multiples of cpr,
+up to the largest index whose rows fit in 2^40 bytes of memory), and that
+the library refuses larger rows."""
+import random
+
+import pytest
+
+MASK64 = (1 << 64) - 1
+
+
+def magic(cpr):
+    return MASK64 // cpr + 1
+
+
+def quotient(n, cpr):
+    return (n * magic(cpr)) >> 64
+
+
+@pytest.mark.parametrize("vec", [4, 8, 16])
+def test_quotient_exact_for_all_row_sizes(vec):
+    rnd = random.Random(vec)
+    max_cpr = (1 << 20) // vec
+    cprs = list(range(2, 2049)) + [max_cpr, max_cpr - 1] + [rnd.randrange(2049, max_cpr) for _ in range(300)]
+    for cpr in cprs:
+        rows_max = (1 << 40) // (cpr * vec)  # rows of cpr * vec bytes that fit in 2^40 bytes
+        for rows in (1, 2, 3, rows_max // 2, rows_max - 1, rows_max, rnd.randrange(1, rows_max + 1)):
+            for n in (rows * cpr - 1, rows * cpr, rows * cpr + cpr - 1):
+                assert quotient(n, cpr) == n // cpr, (cpr, n)
