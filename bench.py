@@ -277,7 +277,7 @@ def main():
         compare([a for a in sys.argv[1:]])
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (each partition's "
+        print("bench.py measures one GPU: the library has no multi-GPU path (each partition's "
               "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
