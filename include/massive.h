@@ -106,8 +106,11 @@ typedef struct {
   void* feat;                              /* [nodes_cap * row_bytes], row i is the
                                               feature row of nodes[i]             */
   int64_t nodes_cap;
-  int32_t* indptr[MASSIVE_MAX_HOPS];       /* hop k: [n[k]+1] offsets into indices */
-  int32_t* indices[MASSIVE_MAX_HOPS];      /* hop k: [e[k]] positions in nodes     */
+  /* entry k (0-based) is the block of hop k+1, which samples for the n[k]
+   * rows of F_k: indptr[k] has n[k]+1 offsets into indices[k], and
+   * indices[k] holds e[k] sampled neighbours as positions in nodes */
+  int32_t* indptr[MASSIVE_MAX_HOPS];
+  int32_t* indices[MASSIVE_MAX_HOPS];
   int64_t indptr_cap[MASSIVE_MAX_HOPS];
   int64_t indices_cap[MASSIVE_MAX_HOPS];
   /* written by massive_sample */
