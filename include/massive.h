@@ -198,7 +198,8 @@ int massive_set_timing(massive_ctx* ctx, int groups);
  * 4 eviction round, 5 refill. Synchronises the context's streams. */
 int massive_get_timing(massive_ctx* ctx, double* out_ms, int64_t* out_calls);
 
-/* Frees every device and host resource of the context. */
+/* Frees every device and host resource of the context; NULL is a no-op.
+ * Always MASSIVE_OK. */
 int massive_destroy(massive_ctx* ctx);
 
 /* Message of the last failure on this context (ctx == NULL: of the last
