@@ -1,12 +1,13 @@
 """The copy kernels flatten (row, 16/8/4-byte chunk) work and recover the row
 of chunk index n as n * magic >> 64 with magic = floor((2^64 - 1) / cpr) + 1,
 cpr the chunks per row. This checks, with exact integers, that the quotient
-is n // cpr for every cpr a row of at most 1 MiB can have, at the chunk
-indices where an error would show first (just below and at multiples of cpr,
-up to the largest index whose rows fit in 2^40 bytes of memory), and that
-the library refuses larger rows (test_abi.py checks that refusal). A model of the flattened loop (U chunks per
-lane per pass) checks that every chunk is stored exactly once and that every
-load, those of lanes past the end included, stays inside the list and the row."""
+is n // cpr for every cpr a row of at most 1 MiB can have (the library
+refuses larger rows; test_abi.py checks that), at the chunk indices where an
+error would show first: just below and at multiples of cpr, up to the
+largest index whose rows fit in 2^40 bytes of memory. A model of the
+flattened loop (U chunks per lane per pass) checks that every chunk is stored
+exactly once and that every load, those of lanes past the end included,
+stays inside the list and the row."""
 import random
 
 import pytest
