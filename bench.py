@@ -246,13 +246,13 @@ def summarize(w, res):
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=192)
-    ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="cl111m_p64")
+    ap.add_argument("--gpus", type=int, default=1, help="GPUs (one partition runs on one GPU: only 1)")
+    ap.add_argument("--steps", type=int, default=192, help="timed minibatches")
+    ap.add_argument("--warmup", type=int, default=8, help="untimed minibatches before them")
+    ap.add_argument("--workload", default="cl111m_p64", help="a named synthetic workload (synth/workloads.py)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle baseline")
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--threads", type=int, default=None)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--threads", type=int, default=None, help="host threads of the input generator")
     ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
     ap.add_argument("--depth", type=int, default=DEFAULT_DEPTH, help="batches in flight (1 to 3)")
     ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
