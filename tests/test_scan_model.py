@@ -4,7 +4,9 @@ interleaving, each publishes its aggregate and then its inclusive prefix in
 one epoch-tagged word, and waits by reading 64 predecessors at a time. The
 model checks that every tile gets the exact exclusive prefix, with stale
 flags of an older epoch present, and that the run ends. It restates the
-kernel's steps; the GPU tests exercise the kernel itself."""
+kernel's steps; the GPU tests exercise the kernel itself. A tile publishes
+its aggregate some time after it starts, so a successor can find its flag
+still holding the older epoch's value and must wait."""
 import random
 
 import pytest
@@ -25,14 +27,17 @@ def run_model(ntiles, seed, start_prob=0.3):
             break
         if pending and (not started or rnd.random() < start_prob):
             b = pending.pop(0)  # blocks start in order
-            flags[b] = ((t_inc if b == 0 else t_agg) << 32) | agg[b]
-            state[b] = [b - 1, 0]
+            state[b] = None     # computing its aggregate: its flag is still an older epoch's
             started.append(b)
             continue
         live = [b for b in started if b not in result]
         if not live:
             continue
         b = rnd.choice(live)
+        if state[b] is None:  # the aggregate is ready: publish it, then look back
+            flags[b] = ((t_inc if b == 0 else t_agg) << 32) | agg[b]
+            state[b] = [b - 1, 0]
+            continue
         p, excl = state[b]
         done = p < 0
         if not done:

@@ -84,3 +84,15 @@ def test_adversarial_start_points():
         tau, cnt, passes, gave_up = search(keys, fo)
         assert passes <= PASSES
         assert gave_up == (not acceptable_exists(keys, fo))
+
+
+def test_a_key_at_tau_is_not_below_it():
+    # four keys below the first tau and one exactly at it: only four are
+    # below, so the search must move on (counting the key at tau would stop
+    # it at a count of five that the candidate list does not hold)
+    fo, d = 5, 300
+    t0 = int(mu(fo) * FULL / d + 1.0)
+    keys = sorted([1, 2, 3, 4, t0] + [FULL - 1 - i for i in range(d - 5)])
+    tau, cnt, passes, gave_up = search(keys, fo)
+    assert gave_up is False and passes > 1
+    assert cnt == bisect.bisect_left(keys, tau) and fo <= cnt <= CAP
