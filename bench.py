@@ -80,6 +80,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     import torch
     from paper_2410_22697_amd import Massive
     depth = depth or DEFAULT_DEPTH
+    warmup = max(1, warmup)  # step 0 runs alone (below)
     torch.cuda.set_device(0)
     t0 = time.time()
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
@@ -113,8 +114,10 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
         if u < 2 and len(first_steps) == u:
             bb = bbs[u % depth]
             nK = r.n[-1]
+            blocks = [(bb.indptr[k][:r.n[k] + 1].cpu().numpy().copy(), bb.indices[k][:r.e[k]].cpu().numpy().copy())
+                      for k in range(len(r.e))]
             first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
-                                bb.feat[:nK].cpu().numpy().copy()))
+                                bb.feat[:nK].cpu().numpy().copy(), blocks))
         if log_steps:
             log("step %d local %d hits %d misses %d rows %d host %d" % (u, r.local, r.hits, r.misses, r.n[-1],
                                                                         r.host_rows))
@@ -133,7 +136,11 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
         for u in inflight:
             finish(u)
 
-    run(0, warmup)
+    # step 0 alone, so that the prefetcher state after it can be read (and
+    # checked against the oracle's); then the rest of the warmup with look-ahead
+    run(0, 1)
+    state0 = gm.state()
+    run(1, warmup)
     log("warmup %d steps done" % warmup)
     r0, e0 = gm.counters()
     f0 = gm.refilled_rows()
@@ -157,7 +164,7 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
                depth=depth,
                stats=np.array(stats, np.float64), sizes=sizes, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
-               refilled=f1 - f0, first_steps=first_steps, tim_prof=tim_prof, stats_prof=stats_prof,
+               refilled=f1 - f0, first_steps=first_steps, state0=state0, tim_prof=tim_prof, stats_prof=stats_prof,
                prof_steps=prof_steps)
     del bbs, seeds_dev
     gm.close()
@@ -323,7 +330,7 @@ def main():
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, res["first_steps"])
+        cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, res["first_steps"], res["state0"])
 
     g_gbps = sm["g_gbps"]
     out = {
@@ -595,10 +602,11 @@ def overlap(w, g, local, store, sched, args):
     gm.close()
 
 
-def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):
+def cpu_baseline(w, g, local, store, sched, budget_s, first_steps, state0=None):
     """The oracle, as it stands, on the same workload from step 0 until the
     budget is spent (at least one step); its first steps are also compared
-    with the GPU's."""
+    with the GPU's, element by element: sizes, frontier, every hop's block,
+    masks and rows, and the prefetcher state after step 0 (bit for bit)."""
     import oracle
     t0 = time.time()
     store_np = store.numpy()
@@ -612,9 +620,16 @@ def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):
         st = orc.sample(sched.seeds(steps))
         orc.evict_step()
         if steps < len(first_steps):
-            r, nodes, mask, feat = first_steps[steps]
+            r, nodes, mask, feat, blocks = first_steps[steps]
             same = (r.n == st.n and r.e == st.e and np.array_equal(nodes, st.nodes) and
-                    np.array_equal(mask, st.mask) and np.array_equal(feat, st.feat))
+                    np.array_equal(mask, st.mask) and np.array_equal(feat, st.feat) and
+                    all(np.array_equal(ip, st.indptr[k]) and np.array_equal(ix, st.indices[k])
+                        for k, (ip, ix) in enumerate(blocks)))
+            if steps == 0 and state0 is not None:
+                sid_o, se_o, sa_o = orc.state()
+                sid_g, se_g, sa_g, _ = state0
+                same = same and (np.array_equal(sid_g, sid_o) and np.array_equal(se_g.view(np.uint32), se_o.view(np.uint32))
+                                 and np.array_equal(sa_g.view(np.uint32), sa_o.view(np.uint32)))
             if not same:
                 raise SystemExit("bench: GPU step %d differs from the oracle" % steps)
             checked += 1
@@ -626,7 +641,8 @@ def cpu_baseline(w, g, local, store, sched, budget_s, first_steps):
     log("oracle: %d steps in %.1fs (%d checked equal to the GPU); phases %s" % (steps, el, checked, np.round(ph, 2)))
     return {"value": round(steps / el, 4), "unit": "minibatches/s", "cores": 1, "kind": "oracle",
             "sample": "steps 0..%d of %s from init (single-threaded C oracle; %d steps compared bit-exact "
-                      "with the GPU run)" % (steps - 1, w.name, checked),
+                      "with the GPU run: sizes, frontier, every hop's block, masks, rows, and the state after "
+                      "step 0)" % (steps - 1, w.name, checked),
             "phase_s_per_step": {k: round(float(v) / steps, 4) for k, v in
                                  zip(("sample", "dedup", "classify", "score", "gather", "evict"), ph)},
             "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}

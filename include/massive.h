@@ -149,7 +149,10 @@ int massive_sample_async(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds
  * back if no later step was issued); MASSIVE_EHIP, and the context refuses
  * further work, if the sampler's threshold search found no acceptable
  * candidate count or a single-pass scan waited past its bound (neither is
- * expected), or if an eviction round produced inconsistent indices. */
+ * expected), or if an eviction round produced inconsistent indices.
+ * MASSIVE_ESTATE for a batch issued after a step that failed in any of these
+ * ways (whichever of the two is waited for first): it was sampled against the
+ * failed step's leftover state, so its outputs are not valid. */
 int massive_batch_wait(massive_ctx* ctx, massive_batch* io);
 
 /* The eviction round owed by the step just sampled; must be called once after

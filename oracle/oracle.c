@@ -8,7 +8,8 @@
  *
  * What it computes, in the paper's order (Algorithm 2, PREFETCH_WITH_EVICTION,
  * and EVICT_AND_REPLACE; scoring rules of Section IV-B; Eq. 1):
- *   initialize_prefetcher (Algorithm 1): BUF = top f% halo nodes by degree,
+ *   initialize_prefetcher (Algorithm 1): BUF = the f share of the halo with
+ *     the largest degrees,
  *     S_E = 1 on BUF, S_A = -1 on BUF and 0 on the other halo nodes,
  *     alpha = gamma^Delta.
  *   NeighborSampler: uniform fanout sampling without replacement, hop by hop
@@ -184,7 +185,8 @@ int oracle_init(const oracle_args* a, oracle_ctx** out) {
     return OR_ENOMEM;
   }
   for (int64_t v = 0; v < R; v++) c->pos[v] = -1;
-  /* halo nodes sorted by degree ("top f% of halo nodes by degree") */
+  /* Algorithm 1 fills the buffer with the highest-degree share f of the halo:
+   * order the halo by degree (ties by global id) */
   int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (size_t)(H ? H : 1));
   if (!order) { oracle_destroy(c); return OR_ENOMEM; }
   for (int64_t h = 0; h < H; h++) order[h] = (int32_t)h;
@@ -193,14 +195,14 @@ int oracle_init(const oracle_args* a, oracle_ctx** out) {
   for (int64_t r = 0; r < H; r++) c->rank[order[r]] = (int32_t)r;
   for (int64_t h = 0; h < H; h++) {
     c->slot_of[h] = -1;
-    c->S_A[h] = 0.0f;                       /* S_A[m] = 0 for halo nodes not in BUF */
+    c->S_A[h] = 0.0f;                       /* Algorithm 1: unbuffered halo nodes start at 0 */
   }
   for (int64_t s = 0; s < c->cap; s++) {
     int32_t h = order[s];
     c->slot_id[s] = h;
     c->slot_of[h] = (int32_t)s;
-    c->S_E[s] = 1.0f;                       /* S_E[n] = 1 */
-    c->S_A[h] = -1.0f;                      /* S_A[n] = -1 */
+    c->S_E[s] = 1.0f;                       /* Algorithm 1: buffered nodes start at 1 */
+    c->S_A[h] = -1.0f;                      /* ... and carry -1 as their S_A */
     memcpy(c->buf + (size_t)s * a->row_bytes,
            (const uint8_t*)a->halo_store + (size_t)h * a->row_bytes, (size_t)a->row_bytes);
   }
@@ -371,13 +373,14 @@ int oracle_sample(oracle_ctx* c, const int32_t* seeds, int32_t n0) {
       else { c->mask[i] = 2; c->misses++; }
     }
     double td = now_s();
-    /* for each n in BUF: if n not sampled, S_E[n] = S_E[n] * gamma */
+    /* Algorithm 2 decay: a buffered node that this step did not sample has
+     * its S_E multiplied by gamma */
     for (int64_t s = 0; s < c->cap; s++) {
       int32_t h = c->slot_id[s];
       int sampled = c->pos[L + h] >= 0;
       if (!sampled) c->S_E[s] = c->S_E[s] * c->a.gamma;
     }
-    /* S_A[n] = S_A[n] + 1 for every n in Misses */
+    /* Algorithm 2 scoring: each missed halo node gains one in S_A */
     for (int64_t i = 0; i < nK; i++)
       if (c->mask[i] == 2) {
         int32_t h = c->F[i] - L;
@@ -418,7 +421,8 @@ static int cmp_cand(const void* pa, const void* pb) {
   int32_t x = *(const int32_t*)pa, y = *(const int32_t*)pb;
   float sx = g_cand_ctx->S_A[x], sy = g_cand_ctx->S_A[y];
   if (sx != sy) return sx > sy ? -1 : 1;
-  return g_cand_ctx->rank[x] < g_cand_ctx->rank[y] ? -1 : 1;
+  int32_t rx = g_cand_ctx->rank[x], ry = g_cand_ctx->rank[y];
+  return rx < ry ? -1 : rx > ry;
 }
 /* eviction order when candidates run short: S_E asc, rank asc */
 static int cmp_evict(const void* pa, const void* pb) {

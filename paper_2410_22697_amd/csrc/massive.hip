@@ -67,6 +67,7 @@ struct massive_ctx {
   int32_t* d_big = nullptr;             // big-row list of the current hop
   int64_t big_min = ms::kBigRow;        // rows longer than this are sampled by a whole block
   int64_t big_blocks = ms::kBigBlocks;  // blocks that walk the list of such rows
+  int32_t tau_iters = ms::kTauIters;    // threshold passes per row (0 makes every long row fail)
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
   // per step slot (step t uses slot t % MASSIVE_MAX_INFLIGHT): classify done
@@ -131,6 +132,7 @@ struct massive_ctx {
   int64_t mat_t = 0;    // S_E materialised through this many steps
   bool pending_round = false;
   bool broken = false;
+  int64_t failed_step = -1;  // earliest step whose batch failed on the device (-1: none)
   struct InFlight {
     massive_batch* io = nullptr;
     int64_t step = -1;
@@ -448,6 +450,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (const char* e = getenv("MASSIVE_REFILL_CHUNKS")) c->refill_chunks = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
   if (const char* e = getenv("MASSIVE_BIG_BLOCKS")) c->big_blocks = std::max<int64_t>(1, atoll(e));
+  if (const char* e = getenv("MASSIVE_TAU_ITERS")) c->tau_iters = std::min(std::max(0, atoi(e)), ms::kTauIters);
   c->s_main = (hipStream_t)a->stream;
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
@@ -718,6 +721,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       sa.big_rows = c->d_big;
       sa.pos_of = c->d_pos_of;
       sa.bits = c->d_bits;
+      sa.tau_iters = c->tau_iters;
       // a small frontier is bound by its longest rows: a block each; a large
       // one keeps the chip busy: a wave each, longest first
       if (nprev <= ms::kBlockRowsMax) {
@@ -830,9 +834,26 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   const massive_ctx::InFlight f = c->infl[slot];
   c->infl[slot] = massive_ctx::InFlight();
   CK(hipEventSynchronize(c->ev_batch_done[slot]));
+  // Steps issued before this one and still in flight decide whether it is
+  // valid: a step that failed on the device skipped its dedup scan and its
+  // classify, so its bitmap marks and frontier positions stayed set, and every
+  // later step sampled against them.
+  for (int i = 0; i < kSlots; ++i)
+    if (c->infl[i].io && c->infl[i].step < f.step) {
+      CK(hipEventSynchronize(c->ev_batch_done[i]));
+      if ((c->h_sz[i].status || c->h_bad[i]) && (c->failed_step < 0 || c->infl[i].step < c->failed_step))
+        c->failed_step = c->infl[i].step;
+    }
+  if (c->failed_step >= 0 && f.step > c->failed_step) {
+    c->broken = true;
+    return c->fail(MASSIVE_ESTATE, "step %lld failed before this batch (step %lld) was complete: its outputs are "
+                                   "not valid and the context is unusable",
+                   (long long)c->failed_step, (long long)f.step);
+  }
   const ms::StepSizes& z = c->h_sz[slot];
   if (c->h_bad[slot]) {
     c->broken = true;
+    c->failed_step = f.step;
     return c->fail(MASSIVE_EHIP, "an eviction round produced inconsistent indices");
   }
   if (z.status & 3) {
@@ -847,10 +868,12 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
       return c->fail(MASSIVE_EINVAL, "%s", why);
     }
     c->broken = true;
+    c->failed_step = f.step;
     return c->fail(MASSIVE_EINVAL, "%s (later work was already issued: context unusable)", why);
   }
   if (z.status) {
     c->broken = true;
+    c->failed_step = f.step;
     return c->fail(MASSIVE_EHIP, "%s (status %d)",
                    (z.status & 8) ? "a single-pass scan waited past its bound" : "sampler could not isolate a candidate set",
                    z.status);

@@ -289,6 +289,7 @@ struct SampleArgs {
   const int32_t* pos_of;    // frontier position of an id, or -1
   uint32_t* bits;           // new-node bitmap
   int32_t* err;             // threshold search could not isolate a candidate set
+  int32_t tau_iters;        // threshold passes allowed per row (kTauIters)
 };
 
 // Philox4x32-10 with counter (q, v, t, hop) for every q of one row. Words 1-3
@@ -504,7 +505,7 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_waves(SampleAr
   bool fail = false, ok = false;
   const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
   const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
-  for (int iter = 0; iter < kTauIters && !fail; ++iter) {
+  for (int iter = 0; iter < a.tau_iters && !fail; ++iter) {
     cnt = 0;
     const uint32_t tm1 = (uint32_t)(ts.tau - 1);  // key < tau  <=>  key <= tau - 1
     for (uint32_t q0 = 0; 4 * q0 < d32; q0 += MS_WAVE) {
@@ -580,7 +581,7 @@ __device__ __forceinline__ void sample_row_wave(const SampleArgs& a, int64_t row
   bool fail = false, ok = false;
   const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
   const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
-  for (int iter = 0; iter < kTauIters && !ok && !fail; ++iter) {
+  for (int iter = 0; iter < a.tau_iters && !ok && !fail; ++iter) {
     cnt = filter_groups(ph, 0, (d32 + 3) / 4, d32, (uint32_t)(ts.tau - 1), c);
     ok = ts.step(cnt, fo, kCandCap, &fail);
   }
@@ -623,7 +624,7 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_blocks(SampleA
       ts.tau = first_tau(a.mu32, d);
       int total = 0;
       bool fail = false, ok = false;
-      for (int iter = 0; iter < kTauIters; ++iter) {
+      for (int iter = 0; iter < a.tau_iters; ++iter) {
         const int cnt = filter_groups(ph, g0, g1, d32, (uint32_t)(ts.tau - 1), cand[wave]);
         if (lane == 0) counts[wave] = cnt;
         __syncthreads();

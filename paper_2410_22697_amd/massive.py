@@ -96,6 +96,22 @@ def _ptr(x) -> Optional[int]:
     return int(x.ctypes.data)
 
 
+def _seed_count(seeds) -> int:
+    """Checks a seed batch before its device pointer goes to the library, which
+    reads it as packed int32 in device memory: a torch int32 tensor on the GPU,
+    contiguous. Returns the number of seeds; raises ValueError otherwise."""
+    import torch
+    if not isinstance(seeds, torch.Tensor):
+        raise ValueError("seeds must be a torch tensor, not %s" % type(seeds).__name__)
+    if seeds.dtype != torch.int32:
+        raise ValueError("seeds must be int32, not %s" % seeds.dtype)
+    if not seeds.is_cuda:
+        raise ValueError("seeds must be a device (cuda) tensor")
+    if seeds.dim() != 1 or not seeds.is_contiguous():
+        raise ValueError("seeds must be a contiguous 1-d tensor")
+    return int(seeds.numel())
+
+
 TIMING_GROUPS = ("sample_dedup", "classify", "gather_hbm", "gather_miss", "evict_round", "refill")
 TIMING_ALL = 0x3F
 
@@ -221,7 +237,7 @@ class Massive:
 
     def sample(self, seeds, bb: BatchBuffers) -> StepResult:
         """seeds: int32 device tensor of distinct local ids."""
-        n0 = int(seeds.numel())
+        n0 = _seed_count(seeds)
         self._check(self._lib.massive_sample(self._h, seeds.data_ptr() if n0 else None, n0,
                                              ctypes.byref(bb.c)))
         c = bb.c
@@ -230,7 +246,7 @@ class Massive:
 
     def sample_async(self, seeds, bb: BatchBuffers) -> None:
         """Enqueues one step; bb must not be touched until wait(bb)."""
-        n0 = int(seeds.numel())
+        n0 = _seed_count(seeds)
         bb._seeds = seeds  # keep the seed tensor alive while the step is in flight
         self._check(self._lib.massive_sample_async(self._h, seeds.data_ptr() if n0 else None, n0,
                                                    ctypes.byref(bb.c)))

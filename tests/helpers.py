@@ -103,3 +103,104 @@ def fp32_decay(x: float, gamma: float, times: int) -> np.float32:
     for _ in range(times):
         v = np.float32(v * g)
     return v
+
+
+# ------------------------------------------------------------------ exact fp32
+# Binary32 rounding written from the IEEE 754 definition with Python integers
+# (fractions), so that it does not depend on the FPU's flush-to-zero or
+# denormals-are-zero modes: round to nearest, ties to even, with gradual
+# underflow (spacing 2^-149 below 2^-126). Non-negative values only, which is
+# all the decay needs.
+from fractions import Fraction  # noqa: E402
+
+_TWO = Fraction(2)
+
+
+def fp32_round(q: Fraction) -> Fraction:
+    """The binary32 value nearest to q >= 0 (ties to even, subnormals kept)."""
+    q = Fraction(q)
+    if q < 0:
+        raise ValueError("non-negative values only")
+    if q == 0:
+        return Fraction(0)
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    if _TWO ** e > q:
+        e -= 1                       # now 2^e <= q < 2^(e+1)
+    ulp = _TWO ** (max(e, -126) - 23)
+    scaled = q / ulp
+    m = scaled.numerator // scaled.denominator
+    rem = scaled - m
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and m % 2 == 1):
+        m += 1
+    return m * ulp
+
+
+def fp32_bits(q: Fraction) -> int:
+    """The bit pattern of a binary32 value given exactly as a fraction."""
+    q = Fraction(q)
+    if q == 0:
+        return 0
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    if _TWO ** e > q:
+        e -= 1
+    if e < -126:                     # subnormal: q = m * 2^-149
+        m = q / _TWO ** -149
+        assert m.denominator == 1 and 0 < m < 2 ** 23
+        return int(m)
+    m = q / _TWO ** (e - 23)
+    assert m.denominator == 1 and 2 ** 23 <= m < 2 ** 24
+    return ((e + 127) << 23) | (int(m) - 2 ** 23)
+
+
+def fp32_decay_exact(x: float, gamma: float, times: int) -> Fraction:
+    """x multiplied `times` times by gamma (both taken as binary32), each
+    product rounded to binary32: the decay's exact result."""
+    g = fp32_round(Fraction(gamma))
+    v = fp32_round(Fraction(x))
+    for _ in range(times):
+        v = fp32_round(v * g)
+    return v
+
+
+def matched_problem(degrees, buffer_pct, gamma, delta, d=4, seed=3) -> Problem:
+    """len(degrees) local nodes, each adjacent to exactly one halo node (local
+    i to halo i), one hop of fanout 1: seeding local i samples halo i and
+    nothing else, so a seed schedule fixes the sampled halo set of every step.
+    halo_degree is given, so it fixes the halo rank order."""
+    n = len(degrees)
+    R = 2 * n
+    indptr = np.arange(R + 1, dtype=np.int64)
+    indices = np.concatenate([np.arange(n, 2 * n), np.arange(n)]).astype(np.int32)
+    rng = np.random.default_rng(seed)
+    feats = rng.standard_normal((R, d)).astype(np.float32)
+    return Problem(n, n, indptr, indices, np.arange(100, 100 + n, dtype=np.int32),
+                   np.asarray(degrees, np.int64), np.ascontiguousarray(feats[:n]),
+                   np.ascontiguousarray(feats[n:]), d, "f32", (1,), buffer_pct, gamma, delta)
+
+
+def subnormal_order_schedule():
+    """Seeds of the scenario in which a halo node whose S_A is subnormal must be
+    chosen ahead of a better-ranked one whose S_A is exactly 0 (six halo nodes
+    h0..h5 ranked in that order, three slots, gamma 0.5, Delta 140, so
+    alpha = 2^-140):
+      step 0: h0, h2 hit, h3 missed (S_A 1); steps 1-140: nothing sampled.
+        Round at 140: h1 (never sampled, S_E 2^-141) is evicted, S_A(h1) =
+        2^-141 (subnormal); h3 replaces it.
+      steps 141-280: h2, h3 hit every step; h5 missed at 141 (S_A 1).
+        Round at 280: h0's S_E has underflowed to exactly 0, so h0 is
+        evicted with S_A(h0) = 0; h5 (S_A 1) replaces it, ahead of h1.
+      steps 281-420: h3, h5 hit. Round at 420: h2's S_E is 0, evicted; the
+        candidates are h0 (S_A 0, rank 0), h1 (S_A 2^-141, rank 1), h4 (S_A 0,
+        rank 4), so h1 replaces it. Flushing subnormals to zero would pick h0.
+    Returns a function t -> seeds (local ids) for t in 0..420."""
+    def seeds(t):
+        if t == 0:
+            return np.array([0, 2, 3], np.int32)
+        if t <= 140:
+            return np.zeros(0, np.int32)
+        if t == 141:
+            return np.array([2, 3, 5], np.int32)
+        if t <= 280:
+            return np.array([2, 3], np.int32)
+        return np.array([3, 5], np.int32)
+    return seeds

@@ -15,7 +15,7 @@ import tempfile
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_philox.py", "tests/test_oracle_sampler.py", "tests/test_oracle_buffer.py",
-        "tests/test_oracle_fuzz.py"]
+        "tests/test_oracle_subnormal.py", "tests/test_oracle_fuzz.py"]
 
 # (label, text in oracle.c, replacement)
 MUTANTS = [
@@ -41,6 +41,14 @@ MUTANTS = [
     ("new nodes not checked against F", "      if (c->pos[u] >= 0) continue;", "      (void)0;"),
     ("short-candidate eviction by S_E descending", "if (ex != ey) return ex < ey ? -1 : 1;",
      "if (ex != ey) return ex > ey ? -1 : 1;"),
+    ("decay flushes subnormal products to zero", "if (!sampled) c->S_E[s] = c->S_E[s] * c->a.gamma;",
+     "if (!sampled) { float x_ = c->S_E[s] * c->a.gamma; c->S_E[s] = x_ < 1.17549435e-38f ? 0.0f : x_; }"),
+]
+# (label, extra gcc flags): the unchanged source built another way. With gcc,
+# -ffast-math also links crtfastmath.o, which sets flush-to-zero and
+# denormals-are-zero for the thread that loads the library.
+FLAG_MUTANTS = [
+    ("built with -ffast-math (flush to zero)", ["-ffast-math"]),
 ]
 # mutants that cannot change any output
 EQUIVALENT = [
@@ -50,7 +58,7 @@ EQUIVALENT = [
 ]
 
 
-def run(label, old, new, tmp):
+def run(label, old, new, tmp, flags=()):
     tree = os.path.join(tmp, "tree")
     shutil.rmtree(tree, ignore_errors=True)
     os.makedirs(tree)
@@ -59,11 +67,12 @@ def run(label, old, new, tmp):
                         ignore=shutil.ignore_patterns("*.so", "__pycache__", ".hypothesis"))
     src = os.path.join(tree, "oracle", "oracle.c")
     text = open(src).read()
-    if text.count(old) != 1:
-        raise SystemExit("mutant %r: the text to replace occurs %d times" % (label, text.count(old)))
-    open(src, "w").write(text.replace(old, new))
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", src, "-o",
-                           os.path.join(tree, "oracle", "liboracle.so")])
+    if old is not None:
+        if text.count(old) != 1:
+            raise SystemExit("mutant %r: the text to replace occurs %d times" % (label, text.count(old)))
+        open(src, "w").write(text.replace(old, new))
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off"] + list(flags) +
+                          [src, "-o", os.path.join(tree, "oracle", "liboracle.so")])
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-p", "no:warnings"]
                        + PINS, cwd=tree, capture_output=True, text=True, timeout=900)
     return r.returncode != 0, (r.stdout.strip().splitlines() or [""])[-1]
@@ -74,6 +83,11 @@ def main():
     with tempfile.TemporaryDirectory() as tmp:
         for label, old, new in MUTANTS:
             caught, last = run(label, old, new, tmp)
+            print("%-45s %s  (%s)" % (label, "caught" if caught else "SURVIVED", last), flush=True)
+            if not caught:
+                survivors.append(label)
+        for label, flags in FLAG_MUTANTS:
+            caught, last = run(label, None, None, tmp, flags)
             print("%-45s %s  (%s)" % (label, "caught" if caught else "SURVIVED", last), flush=True)
             if not caught:
                 survivors.append(label)

@@ -103,3 +103,20 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(massive, "_lib", None)
     with pytest.raises(ImportError):
         massive.load()
+
+
+def test_seed_tensor_is_checked_before_the_library_reads_it():
+    """The library reads seeds as packed int32 device memory: an int64, host or
+    strided tensor is refused in the binding, before any library call."""
+    import torch
+    from paper_2410_22697_amd.massive import _seed_count
+    with pytest.raises(ValueError, match="int32"):
+        _seed_count(torch.zeros(4, dtype=torch.int64))
+    with pytest.raises(ValueError, match="device"):
+        _seed_count(torch.zeros(4, dtype=torch.int32))
+    with pytest.raises(ValueError, match="torch tensor"):
+        _seed_count([1, 2, 3])
+    if torch.cuda.is_available():
+        with pytest.raises(ValueError, match="contiguous"):
+            _seed_count(torch.arange(8, dtype=torch.int32, device="cuda")[::2])
+        assert _seed_count(torch.arange(5, dtype=torch.int32, device="cuda")) == 5

@@ -94,8 +94,9 @@ def test_lookahead_round_every_step(depth):
 
 def test_invalid_seeds_with_later_steps_in_flight():
     # a step whose seeds are invalid cannot be taken back once a later step
-    # was issued: its wait reports the seeds and the context refuses further
-    # work; the batches around it complete normally (no kernel waits on it)
+    # was issued: its wait reports the seeds, the batch issued after it is
+    # refused (it ran at a step count the failed step had already advanced),
+    # and the context refuses further work; every kernel completes normally
     from paper_2410_22697_amd import MassiveError
     prob, sched, w = workload_problem("cl10k")
     gm = make_gpu(prob)
@@ -108,10 +109,65 @@ def test_invalid_seeds_with_later_steps_in_flight():
     with pytest.raises(MassiveError) as ei:
         gm.wait(bbs[1])
     assert ei.value.code == -1
-    gm.wait(bbs[2])
+    with pytest.raises(MassiveError) as ei:
+        gm.wait(bbs[2])
+    assert ei.value.code == -5
     with pytest.raises(MassiveError) as ei:
         gm.sample_async(seeds[0], bbs[0])
     assert ei.value.code == -5
+
+
+@pytest.mark.parametrize("order", ["in order", "later batch first"])
+def test_failed_step_invalidates_later_batches(order, monkeypatch):
+    # A step that fails on the device (here forced from the host: zero
+    # threshold passes make every row longer than its fanout report a failed
+    # search; every kernel still exits normally) skips its dedup scan and
+    # classify, leaving bitmap marks and frontier positions set that later
+    # steps sample against. The batch before it stays valid; the failed one
+    # reports EHIP; every batch issued after it reports ESTATE, whichever is
+    # waited for first; the context then refuses further work.
+    from paper_2410_22697_amd import MassiveError
+    prob, sched, w = workload_problem("cl10k")
+    gm_ok = make_gpu(prob)
+    monkeypatch.setenv("MASSIVE_TAU_ITERS", "0")
+    gm = make_gpu(prob)
+    monkeypatch.delenv("MASSIVE_TAU_ITERS")
+    orc = prob.oracle()
+    bbs = [gm.alloc_batch(w.batch) for _ in range(3)]
+    seeds = [to_dev(sched.seeds(t)) for t in range(3)]
+    # step 0 with an empty batch (nothing to sample: valid), then two full ones
+    empty = to_dev(np.zeros(0, np.int32))
+    log("failed step test (%s): enqueue" % order)
+    gm.sample_async(empty, bbs[0])
+    gm.evict_step(wait=False)
+    for t in (1, 2):
+        gm.sample_async(seeds[t], bbs[t])
+        gm.evict_step(wait=False)
+    res0 = gm.wait(bbs[0])
+    st0 = orc.sample(np.zeros(0, np.int32))
+    compare_step("failed-step test t=0", st0, res0, bbs[0], len(prob.fanout))
+    if order == "in order":
+        with pytest.raises(MassiveError) as ei:
+            gm.wait(bbs[1])
+        assert ei.value.code == -4
+        with pytest.raises(MassiveError) as ei:
+            gm.wait(bbs[2])
+        assert ei.value.code == -5
+    else:
+        with pytest.raises(MassiveError) as ei:
+            gm.wait(bbs[2])
+        assert ei.value.code == -5
+        with pytest.raises(MassiveError) as ei:
+            gm.wait(bbs[1])
+        assert ei.value.code == -4
+    with pytest.raises(MassiveError) as ei:
+        gm.sample_async(seeds[0], bbs[0])
+    assert ei.value.code == -5
+    gm.close()
+    # a context made without the limit samples normally
+    bb = gm_ok.alloc_batch(w.batch)
+    orc2 = prob.oracle()
+    compare_step("control t=0", orc2.sample(sched.seeds(0)), gm_ok.sample(seeds[0], bb), bb, len(prob.fanout))
 
 
 def test_lookahead_rejects_one_batch_too_many():

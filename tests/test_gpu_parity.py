@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from gpu_util import log, make_gpu, pinned_store, require_gpu, run_parity, to_dev
-from helpers import tiny_problem, workload_problem
+from helpers import matched_problem, subnormal_order_schedule, tiny_problem, workload_problem
 
 pytestmark = pytest.mark.gpu
 
@@ -68,6 +68,50 @@ def test_cl2m45_bf16_rows():
     sch = Schedule(prob.L, w.train_pct, 512, w.seed)
     rounds, _, _ = run_parity("cl2m45_bf16", prob, sch.seeds, 5, state_every=2)
     assert rounds == 1
+
+
+@pytest.mark.timeout(900)
+def test_cl2m45_bf16_stated_batch():
+    # the stated shape: batch 4096, fanout (20,15,10), bf16 rows, f 50%,
+    # gamma 0.8, Delta 4; every step element by element through the first
+    # round (after t = 4) and two steps after it (the oracle takes ~10 s a step)
+    prob, sched, w = workload_problem("cl2m45_bf16")
+    assert w.batch == 4096
+    rounds, _, _ = run_parity("cl2m45_bf16 batch 4096", prob, sched.seeds, 7, state_every=1, buffer_rows_every=4)
+    assert rounds == 1
+
+
+def _subnormals(x):
+    return int(((x > 0) & (x < np.float32(2.0 ** -126))).sum())
+
+
+def test_subnormal_scores_cl10k():
+    # gamma 0.3, Delta 80: alpha = 0.3^80 is subnormal, unsampled slots' S_E
+    # pass through 2^-126..2^-149 to 0, and the round at t = 160 moves
+    # subnormal S_E into S_A (the swap of Section IV-B). S_E and S_A bits are
+    # compared after every one of 241 steps (rounds at 80, with nothing below
+    # alpha yet, 160 and 240).
+    prob, sched, w = workload_problem("cl10k", gamma=0.3, delta=80)
+    orc, gm = prob.oracle(), make_gpu(prob)
+    assert 0 < np.float32(orc.alpha) < np.float32(2.0 ** -126)
+    r1, _, _ = run_parity("cl10k subnormal", prob, sched.seeds, 161, gm=gm, orc=orc)
+    _, se, sa = orc.state()
+    assert r1 >= 1 and _subnormals(se) > 0 and _subnormals(sa) > 0
+    r2, _, _ = run_parity("cl10k subnormal, steps 161-240", prob, lambda t: sched.seeds(161 + t), 80, gm=gm, orc=orc)
+    assert r2 >= 1
+
+
+def test_subnormal_S_A_outranks_zero():
+    # a candidate whose S_A is subnormal (2^-141, from a swap) must be chosen
+    # ahead of a better-ranked candidate whose S_A is exactly 0: the three
+    # rounds of helpers.subnormal_order_schedule, state bits after every step
+    prob = matched_problem([6, 5, 4, 3, 2, 1], buffer_pct=50, gamma=0.5, delta=140)
+    orc, gm = prob.oracle(), make_gpu(prob)
+    rounds, _, _ = run_parity("subnormal order", prob, subnormal_order_schedule(), 421, gm=gm, orc=orc,
+                              batch_max=3)
+    assert rounds == 3
+    sid, se, _, _ = gm.state()
+    assert sid.tolist() == [5, 3, 1] and int(se.view(np.uint32)[2]) == 1 << 8
 
 
 def test_empty_and_ragged_batches():
