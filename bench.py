@@ -5,12 +5,23 @@
 A step is one minibatch through the whole path: massive_sample (3-hop fanout
 sampling, dedup/relabel, buffer lookup, scoring, HBM gather, miss fetch from
 pinned host memory) followed by massive_evict_step (the periodic eviction
-and replacement round, with its refill overlapping the next step). Inputs
-(graph, features, seed batches) are resident before the timed region.
+and replacement round, with its refill overlapping the next steps). Inputs
+(graph, features, seed batches) are resident before any timed region.
 
-Prints one JSON line: minibatches/s, the gather kernel against the HBM
-roofline, the hit rate, the host-link rate of the miss fetch, and the CPU
-oracle timed on a bounded sample of the same workload.
+Prints one JSON line for the papers-sized share (cl111m_p64):
+  - value: minibatches/s over `--steps` steps that lie after the first
+    eviction round and contain a round (the eviction regime; the window rule
+    is in window_plan), with the gather kernel against the HBM roofline, the
+    miss fetch against the host link, and the bound of the whole minibatch
+    computed from measured fractions;
+  - early_window: the `--steps` steps right after warm-up (before any round
+    for a short window: the initial buffer only);
+  - eviction_run: a fresh context from init through five rounds, every
+    kernel group timed over its own steps, with the per-step hit rate;
+  - sampler: the last hop's sampler kernel against the VALU issue rate;
+  - configs: the four smaller workloads, their stated runs and the extended
+    runs of those whose stated run reaches no round (child processes);
+  - cpu_baseline: the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -24,29 +35,27 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
-# Batches in flight in the timed loop (the library allows up to three): with
-# two, the next step's sampling overlaps the current step's host-link reads
-# and never the HBM gather; a third lets sampling run beside the HBM gather
-# too, which slows it, with no gain while the host link bounds the step.
-DEFAULT_DEPTH = 2
 PCIE_PEAK_GBPS = 64.0        # PCIe 5.0 x16, one direction
-
-
-def gather_traffic(rb_per_launch):
-    """HBM bytes per gather_hbm launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), as a ratio to
-    the algorithmic bytes applied to this run's launches; None if the gather
-    kernel's source has changed since the counters were taken."""
-    import hashlib
-    prof = os.path.join(ROOT, "profiles", "gather_hbm_cl111m_p64_hbm_counters.txt")
-    src = open(os.path.join(ROOT, "paper_2410_22697_amd", "csrc", "buffer_kernels.hpp")).read()
-    a, b = src.find("// ---------------------------------------------------------------- gather"), src.find("// misses: pinned host store")
-    if not os.path.exists(prof) or a < 0 or b < 0:
-        return None
-    kv = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if l.startswith(("traffic_", "gather_source")))
-    if kv.get("gather_source_sha256") != hashlib.sha256(src[a:b].encode()).hexdigest():
-        return None
-    return round(float(kv["traffic_over_algorithmic"]) * rb_per_launch)
+LINK_CEILING_GBPS = 55.0     # measured: zero-copy row reads of a pinned store by 16 blocks
+# Batches in flight (the library allows up to three): with two, the next
+# step's sampling overlaps the current step's host-link reads and never the
+# HBM gather; a third lets sampling run beside the HBM gather too, which
+# slows it, with no gain while the host link bounds the step.
+DEFAULT_DEPTH = 2
+# VALU issue peak of the sampler, in Philox keys per second: 256 CUs issue one
+# wave64 VALU instruction per clock each (four SIMDs, four clocks per wave64
+# instruction) at 2.4 GHz; one pass of the sampler's inner loop is 42 VALU
+# instructions for 64 Philox4x32-10 blocks = 256 keys (the block function's
+# 20 multiplies and 20 three-way XORs less the two hoisted products, plus the
+# below-threshold test).
+SAMPLER_VALU_PER_256_KEYS = 42
+SAMPLER_PEAK_KEYS_PER_S = 256 * 2.4e9 * 256 / SAMPLER_VALU_PER_256_KEYS
+EVICTION_RUN_ROUNDS = 5      # the eviction run covers steps 0 .. 5 delta
+SAMPLER_STEPS = 16           # steps of the sampler measurement
+# the smaller workloads: stated runs, and extended runs (four rounds) for
+# those whose stated run ends before the first round
+CONFIG_GROUPS = (("cl10k", "cl170k"), ("cl2m45",), ("cl2m45_bf16",))
+EXTENDED_ROUNDS = 4
 
 
 def log(msg):
@@ -70,28 +79,64 @@ def build_inputs(w, threads=None):
     return g, local, store, sched
 
 
-def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_probe=False, depth=None,
-                timed_groups=("gather_hbm",), prof_steps=64):
-    """One context over steps 0..warmup+steps-1 with look-ahead (`depth`
-    batches in flight); the last `steps` are timed, with HIP events only on
-    `timed_groups` (every timed group adds event packets to the streams).
-    Then `prof_steps` further steps with every group timed give the phase
-    breakdown. Returns the raw measurements."""
+def window_plan(warmup, steps, delta, limit=20000):
+    """The two timed windows of the default run, each [start, stop):
+    early = the `steps` steps right after warm-up (before the first round when
+    warmup + steps <= delta + 1); headline = `steps` steps after the first
+    round (t = delta), so that refill traffic is in its steady state, that
+    contain a round: a window shorter than delta is centred on a round at
+    2 delta or later; a longer one starts right after the first round (any
+    delta consecutive steps hold a round). The headline never overlaps the
+    early window. An interval too long for this (a static buffer) gives the
+    early window only (headline = early)."""
+    warmup = max(1, warmup)  # step 0 runs alone
+    early = (warmup, warmup + steps)
+    if 2 * delta + 2 * steps + warmup > limit:
+        return early, early
+    if steps >= delta:
+        s = max(warmup + steps, delta + 1)
+    else:
+        r = delta * max(2, -(-(warmup + steps + steps // 2) // delta))
+        s = r - steps // 2
+    return early, (s, s + steps)
+
+
+def frontier_keys(indptr, nodes, fanout):
+    """Philox keys one hop draws by definition: d keys for every frontier row
+    longer than the fanout (shorter rows are copied whole)."""
+    d = indptr[nodes + 1] - indptr[nodes]
+    return int(d[d > fanout].sum())
+
+
+def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False, copy_probe=False,
+                first_alone=True, sampler_steps=0):
+    """One context from init over steps 0..end-1 with look-ahead (`depth`
+    batches in flight: step t is enqueued, after step t-1's round, before step
+    t - depth + 1 is waited for, so the sampling of the next steps overlaps the
+    host-link reads of earlier ones).
+    first_alone: step 0 runs alone first, and its outputs and the state after
+    it are kept for the oracle check.
+    windows: (label, start, stop, groups), in step order: steps [start, stop)
+    are timed on the host clock between two synchronisations, with HIP events
+    on the kernel groups `groups` (True: every group); steps between windows
+    run untimed.
+    sampler_steps: that many more steps time the last hop's sampler dispatch
+    and count its keys on the host (each step's frontier is copied back,
+    which holds the pipeline a little)."""
     import torch
     from paper_2410_22697_amd import Massive
     depth = depth or DEFAULT_DEPTH
-    warmup = max(1, warmup)  # step 0 runs alone (below)
     torch.cuda.set_device(0)
+    end = max([1] + [b for _, _, b, _ in windows])
+    total = end + sampler_steps
     t0 = time.time()
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
                  w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
     torch.cuda.synchronize()
     init_s = time.time() - t0
-    log("massive_init %.2fs: cap=%d alpha=%.6g" % (init_s, gm.cap, gm.alpha))
+    log("%s: massive_init %.2fs: cap=%d alpha=%.6g" % (w.name, init_s, gm.cap, gm.alpha))
     bbs = [gm.alloc_batch(w.batch) for _ in range(depth)]
-    total = warmup + steps
-    seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda()
-                 for t in range(total + prof_steps)]
+    seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
     torch.cuda.synchronize()
 
     if copy_probe:
@@ -106,28 +151,31 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
     first_steps = []  # the first steps' outputs, checked against the oracle
     stats = []        # per step: local, hits, misses, rows, host-link rows
     sizes = []        # per step: frontier sizes n_0..n_K and sampled edges e_1..e_K
+    keys = []         # per sampler step: keys of the last hop
+    count_keys = [False]
+    K = len(w.fanout)
 
     def finish(u):
-        r = gm.wait(bbs[u % depth])
+        bb = bbs[u % depth]
+        r = gm.wait(bb)
         stats.append((r.local, r.hits, r.misses, r.n[-1], r.host_rows))
         sizes.append((list(r.n), list(r.e)))
-        if u < 2 and len(first_steps) == u:
-            bb = bbs[u % depth]
+        if first_alone and u < 2 and len(first_steps) == u:
             nK = r.n[-1]
             blocks = [(bb.indptr[k][:r.n[k] + 1].cpu().numpy().copy(), bb.indices[k][:r.e[k]].cpu().numpy().copy())
-                      for k in range(len(r.e))]
+                      for k in range(K)]
             first_steps.append((r, bb.nodes[:nK].cpu().numpy().copy(), bb.mask[:nK].cpu().numpy().copy(),
                                 bb.feat[:nK].cpu().numpy().copy(), blocks))
+        if count_keys[0]:
+            keys.append(frontier_keys(g.indptr, bb.nodes[:r.n[K - 1]].cpu().numpy().astype(np.int64),
+                                      w.fanout[-1]))
         if log_steps:
             log("step %d local %d hits %d misses %d rows %d host %d" % (u, r.local, r.hits, r.misses, r.n[-1],
                                                                         r.host_rows))
 
-    def run(t0, t1):
-        """Steps t0..t1-1 with look-ahead: step t is enqueued (after step t-1's
-        round) before step t - depth + 1 is waited for, so the sampling of the
-        next steps overlaps the host-link reads of earlier ones."""
+    def run(a, b):
         inflight = []
-        for t in range(t0, t1):
+        for t in range(a, b):
             gm.sample_async(seeds_dev[t], bbs[t % depth])
             gm.evict_step(wait=False)
             inflight.append(t)
@@ -136,38 +184,48 @@ def run_context(w, g, local, store, sched, warmup, steps, log_steps=False, copy_
         for u in inflight:
             finish(u)
 
-    # step 0 alone, so that the prefetcher state after it can be read (and
-    # checked against the oracle's); then the rest of the warmup with look-ahead
-    run(0, 1)
-    state0 = gm.state()
-    run(1, warmup)
-    log("warmup %d steps done" % warmup)
-    r0, e0 = gm.counters()
-    f0 = gm.refilled_rows()
-    gm.set_timing(timed_groups)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run(warmup, total)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    tim = gm.timing()
-    r1, e1 = gm.counters()
-    f1 = gm.refilled_rows()
-    tim_prof, stats_prof = None, None
-    if prof_steps:
-        n_timed = len(stats)
-        gm.set_timing(True)
-        run(total, total + prof_steps)
-        tim_prof = gm.timing()
-        stats_prof = np.array(stats[n_timed:], np.float64)
-        del stats[n_timed:], sizes[n_timed:]
-    out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, elapsed=elapsed, steps=steps, warmup=warmup,
-               depth=depth,
-               stats=np.array(stats, np.float64), sizes=sizes, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
-               refilled=f1 - f0, first_steps=first_steps, state0=state0, tim_prof=tim_prof, stats_prof=stats_prof,
-               prof_steps=prof_steps)
+    state0 = None
+    pos = 0
+    if first_alone:
+        run(0, 1)
+        state0 = gm.state()
+        pos = 1
+    out_w = {}
+    for label, a, b, groups in windows:
+        assert a >= pos and b > a, (label, a, b, pos)
+        run(pos, a)
+        r0, e0 = gm.counters()
+        f0 = gm.refilled_rows()
+        gm.set_timing(groups)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(a, b)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        tim = gm.timing()
+        r1, e1 = gm.counters()
+        f1 = gm.refilled_rows()
+        gm.set_timing(False)
+        out_w[label] = dict(start=a, stop=b, elapsed=el, tim=tim, rounds=r1 - r0, evicted=e1 - e0,
+                            refilled=f1 - f0, groups=groups)
+        log("%s %s: steps %d..%d in %.4fs: %.1f minibatches/s, %d rounds" % (w.name, label, a, b - 1, el,
+                                                                          (b - a) / el, r1 - r0))
+        pos = b
+    sampler = None
+    if sampler_steps:
+        gm.set_timing(["sample_last_hop"])
+        count_keys[0] = True
+        run(pos, pos + sampler_steps)
+        count_keys[0] = False
+        ms, calls = gm.timing()["sample_last_hop"]
+        sampler = dict(ms=ms, calls=calls, keys=list(keys), steps=(pos, pos + sampler_steps))
+        gm.set_timing(False)
+    out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, depth=depth,
+               stats=np.array(stats, np.float64), sizes=sizes, windows=out_w,
+               first_steps=first_steps, state0=state0, sampler=sampler)
     del bbs, seeds_dev
     gm.close()
+    torch.cuda.synchronize()
     return out
 
 
@@ -214,59 +272,214 @@ def alg_hbm_bytes(n, e, loc, hit, mis, rb):
     return b + 13 * n[-1] + 2 * (loc + hit) * rb + mis * rb + 8 * (mis + hit)
 
 
-def summarize(w, res):
-    """Throughput, the gather against the HBM roofline, the host link, the hit rate."""
-    K, rb = res["steps"], w.row_bytes
-    st = res["stats"][res["warmup"]:]
+MAIN_STREAM_GROUPS = ("sample_dedup", "classify")
+
+
+def summarize(w, res, label):
+    """One timed window: throughput, the gather against the HBM roofline, the
+    miss fetch against the host link, the hit rate, and the bound of the whole
+    minibatch, taken as the largest of three measured fractions: HBM
+    (algorithmic bytes per second over 8 TB/s), host link (bytes that crossed
+    it per second over 64 GB/s) and the main stream (the share of the step its
+    sampling, dedup and classify kernels occupy, when those groups are timed)."""
+    win = res["windows"][label]
+    a, b = win["start"], win["stop"]
+    K, rb = b - a, w.row_bytes
+    st = res["stats"][a:b]
     loc, hit, mis, host_rows = st[:, 0], st[:, 1], st[:, 2], st[:, 4]
     hbm_rows = loc + hit
-    tim = res["tim"]
-    mbps = K / res["elapsed"]
-    # gather_hbm algorithmic bytes: read + write each HBM-sourced row, plus its 8-byte list entry
+    tim = win["tim"]
+    el = win["elapsed"]
+    mbps = K / el
     g_ms, g_calls = tim["gather_hbm"]
     g_bytes = float(np.mean(2 * hbm_rows * rb + 8 * hbm_rows))
-    g_avg_s = g_ms / 1e3 / max(g_calls, 1)
-    # the miss gather's own rate: from the steps with every group timed, if any
-    if res.get("tim_prof"):
-        m_ms, m_calls = res["tim_prof"]["gather_miss"]
-        m_bytes = float(np.mean(res["stats_prof"][:, 4] * rb))
-    else:
-        m_ms, m_calls = tim["gather_miss"]
-        m_bytes = float(np.mean(host_rows * rb))
-    refill_bytes = res["refilled"] * rb / max(K, 1)  # copied by refill chunks inside the timed region, per step
-    sz = res["sizes"][res["warmup"]:]
+    g_avg_s = g_ms / 1e3 / g_calls if g_calls else None
+    m_ms, m_calls = tim["gather_miss"]
+    m_bytes = float(np.mean(host_rows * rb))
+    sz = res["sizes"][a:b]
     b_alg = float(np.mean([alg_hbm_bytes(n, e, l, h, m, rb) for (n, e), (l, h, m) in zip(sz, st[:, :3])]))
     # eviction rounds, amortised: S_E/slot scans and S_A/rank scans, and the replacement rows written
-    b_alg += (res["rounds"] * (12 * res["gm_cap"] + 8 * res["H"]) + res["evicted"] * rb) / max(K, 1)
-    link_bytes = float(np.mean(host_rows * rb)) + refill_bytes
-    return dict(mbps=mbps, b_alg=b_alg, link_bytes=link_bytes, g_bytes=g_bytes, g_avg_s=g_avg_s, g_gbps=g_bytes / g_avg_s / 1e9,
-                m_bytes=m_bytes, m_avg_us=1e3 * m_ms / max(m_calls, 1),
-                m_gbps=m_bytes / (m_ms / 1e3 / max(m_calls, 1)) / 1e9 if m_ms > 0 else 0.0,
-                hit_rate=float(hit.sum() / max(hit.sum() + mis.sum(), 1)),
-                pend_bytes=float(np.mean((host_rows - mis) * rb)), refill_bytes=refill_bytes,
-                host_bytes=float(np.mean(host_rows * rb)),
-                evicted_bytes=res["evicted"] * rb / max(K, 1),
-                link_gbps=(float(host_rows.sum()) * rb + res["refilled"] * rb) / res["elapsed"] / 1e9,
-                remote_rows=float(np.mean(host_rows)) + res["refilled"] / max(K, 1),
-                halo_rows=float(np.mean(hit + mis)))
+    b_alg += (win["rounds"] * (12 * res["gm_cap"] + 8 * res["H"]) + win["evicted"] * rb) / K
+    link_bytes = float(host_rows.sum()) * rb + win["refilled"] * rb
+    link_gbps = link_bytes / el / 1e9
+    hbm_gbps = mbps * b_alg / 1e9
+    phases = {k: round(v[0] / K, 4) for k, v in tim.items() if v[1]}
+    fr = {"hbm": hbm_gbps / HBM_PEAK_GBPS, "host_link": link_gbps / PCIE_PEAK_GBPS}
+    main_ms = None
+    if all(tim[gname][1] for gname in MAIN_STREAM_GROUPS):
+        main_ms = sum(tim[gname][0] for gname in MAIN_STREAM_GROUPS) / K
+        fr["main_stream"] = main_ms / (1e3 * el / K)
+    bound = max(fr, key=fr.get)
+    out = {
+        "steps_timed": [a, b - 1], "eviction_rounds": win["rounds"], "evicted_rows": win["evicted"],
+        "refilled_rows": win["refilled"],
+        "value": round(mbps, 3), "unit": "minibatches/s", "ms_per_step": round(1e3 * el / K, 4),
+        "hit_rate": round(float(hit.sum() / max(hit.sum() + mis.sum(), 1)), 4),
+        "gather_hbm": None if g_avg_s is None else {
+            "bytes_per_launch": round(g_bytes), "avg_us": round(g_avg_s * 1e6, 2),
+            "GBps": round(g_bytes / g_avg_s / 1e9, 1), "frac_hbm": round(g_bytes / g_avg_s / 1e9 / HBM_PEAK_GBPS, 4)},
+        "gather_miss": None if not m_calls else {
+            "bytes_per_launch": round(m_bytes), "avg_us": round(1e3 * m_ms / m_calls, 2),
+            "GBps": round(m_bytes / (m_ms / 1e3 / m_calls) / 1e9, 2) if m_ms > 0 else None},
+        "minibatch_roofline": {
+            "bound": {"hbm": "hbm", "host_link": "host link", "main_stream": "main stream (sampling, dedup, classify)"}[bound],
+            "fractions": {k: round(v, 4) for k, v in fr.items()},
+            "hbm_alg_bytes_per_step": round(b_alg), "hbm_GBps": round(hbm_gbps, 1),
+            "link_bytes_per_step": round(link_bytes / K), "link_GBps": round(link_gbps, 2),
+            "link_peak_GBps": PCIE_PEAK_GBPS, "link_ceiling_measured_GBps": LINK_CEILING_GBPS,
+            "main_stream_ms_per_step": None if main_ms is None else round(main_ms, 4)},
+        "host_rows_per_step": round(float(np.mean(host_rows)), 1),
+        "refill_rows_per_step": round(win["refilled"] / K, 1),
+        "remote_rows_per_step": round(float(np.mean(host_rows)) + win["refilled"] / K, 1),
+        "halo_rows_per_step": round(float(np.mean(hit + mis)), 1),
+        "phase_ms_per_step": phases,
+        "phases_timed": "every kernel group" if win["groups"] is True else list(win["groups"] or []),
+    }
+    return out
+
+
+def gather_traffic(window, workload):
+    """HBM bytes per gather_hbm launch over the headline window, measured by
+    rocprofv3 counters (FETCH_SIZE, then WRITE_SIZE, scaled by a plain copy)
+    on the same command, from the committed summary; None unless the summary
+    covers this workload and window and the gather kernel's source is the one
+    the counters were taken on."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "gather_hbm_%s_hbm_counters.txt" % workload)
+    src = open(os.path.join(ROOT, "paper_2410_22697_amd", "csrc", "buffer_kernels.hpp")).read()
+    a, b = src.find("// ---------------------------------------------------------------- gather"), src.find("// misses: pinned host store")
+    if not os.path.exists(prof) or a < 0 or b < 0:
+        return None
+    kv = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if ": " in l and not l.startswith(" "))
+    if kv.get("gather_source_sha256") != hashlib.sha256(src[a:b].encode()).hexdigest():
+        return None
+    if kv.get("window_steps") != "%d..%d" % (window[0], window[1] - 1):
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
+def sampler_summary(res, w):
+    s = res["sampler"]
+    if not s or not s["calls"]:
+        return None
+    keys = float(np.mean(s["keys"]))
+    avg_s = s["ms"] / 1e3 / s["calls"]
+    kps = keys / avg_s
+    return {"kernel": "k_sample_waves (hop %d)" % len(w.fanout), "bound": "alu", "steps": list(s["steps"]),
+            "keys_per_launch": round(keys), "avg_us": round(avg_s * 1e6, 2), "achieved": round(kps / 1e12, 4),
+            "peak": round(SAMPLER_PEAK_KEYS_PER_S / 1e12, 4), "unit": "T keys/s",
+            "frac": round(kps / SAMPLER_PEAK_KEYS_PER_S, 4),
+            "peak_from": "256 CUs x 2.4 GHz x 1 wave64 VALU instruction per clock x 256 keys per %d instructions"
+                         % SAMPLER_VALU_PER_256_KEYS,
+            "keys_from": "sum of row lengths over the hop's frontier rows longer than the fanout (one Philox "
+                         "key per position), counted on the host from the same steps"}
+
+
+def config_entry(w, res, label, kind):
+    """A compact record of one run of a smaller workload."""
+    sm = summarize(w, res, label)
+    g = sm["gather_hbm"]
+    mr = sm["minibatch_roofline"]
+    return {"kind": kind, "steps": res["windows"][label]["stop"], "from_init": True,
+            "value": sm["value"], "unit": "minibatches/s", "ms_per_step": sm["ms_per_step"],
+            "eviction_rounds": sm["eviction_rounds"], "evicted_rows": sm["evicted_rows"],
+            "hit_rate": sm["hit_rate"], "gather_frac_hbm": g["frac_hbm"] if g else None,
+            "gather_GBps": g["GBps"] if g else None, "link_GBps": mr["link_GBps"],
+            "bound": mr["bound"], "fractions": mr["fractions"], "init_s": round(res["init_s"], 3)}
+
+
+def config_run(names, args):
+    """Child mode: the smaller workloads' runs, one JSON line per workload.
+    A workload whose stated run reaches no round (its run is shorter than
+    delta + 1) also gets an extended run of four rounds. Every run is one
+    context from init, timed from step 0 to its end with every kernel group
+    timed. The 10K-node workload's stated run is short enough for the oracle:
+    it is timed in full and its per-step sizes and counts compared."""
+    import synth
+    for name in names:
+        w = synth.get(name)
+        g, local, store, sched = build_inputs(w, args.threads)
+        entry = {"workload": name, "stands_in_for": w.note or None, "nodes": w.n, "partitions": w.parts,
+                 "L": g.L, "H": g.H, "csr_entries": g.nnz, "batch": w.batch, "fanout": list(w.fanout),
+                 "row_bytes": w.row_bytes, "dtype": w.dtype, "buffer_pct": w.buffer_pct, "gamma": w.gamma,
+                 "delta": w.delta, "runs": []}
+        lengths = [("stated", w.steps)]
+        if w.steps < w.delta + 1:
+            lengths.append(("extended", EXTENDED_ROUNDS * w.delta + 1))
+        for kind, n in lengths:
+            res = run_context(w, g, local, store, sched, [("run", 0, n, True)], first_alone=False)
+            e = config_entry(w, res, "run", kind)
+            if kind == "stated" and name == "cl10k" and not args.no_cpu:
+                e["cpu_baseline"] = oracle_full_run(w, g, local, store, sched, n, res)
+            entry["runs"].append(e)
+            log("%s %s run: %d steps, %.1f minibatches/s, %d rounds, hit rate %.3f" %
+                (name, kind, n, e["value"], e["eviction_rounds"], e["hit_rate"]))
+        print(json.dumps(entry), flush=True)
+
+
+def oracle_full_run(w, g, local, store, sched, n, res):
+    """The oracle over a whole stated run, timed; each step's sizes and class
+    counts are compared with the GPU run's."""
+    import oracle
+    orc = oracle.Oracle(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store.numpy(),
+                        w.row_bytes, w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
+    t0 = time.perf_counter()
+    for t in range(n):
+        st = orc.sample(sched.seeds(t))
+        orc.evict_step()
+        (gn, ge), row = res["sizes"][t], res["stats"][t]
+        if gn != st.n or ge != st.e or (int(row[0]), int(row[1]), int(row[2])) != (st.local, st.hits, st.misses):
+            raise SystemExit("bench: %s step %d differs from the oracle" % (w.name, t))
+    el = time.perf_counter() - t0
+    return {"value": round(n / el, 3), "unit": "minibatches/s", "cores": 1, "kind": "oracle",
+            "sample": "the whole %d-step run from init; every step's sizes and class counts equal the GPU's" % n}
+
+
+def configs_in_children(args):
+    """Runs the smaller workloads in child processes (at most two contexts
+    each) and collects their lines."""
+    import subprocess
+    out = []
+    for group in CONFIG_GROUPS:
+        cmd = [sys.executable, os.path.abspath(__file__), "--config-run", ",".join(group)]
+        if args.no_cpu:
+            cmd.append("--no-cpu")
+        if args.threads:
+            cmd += ["--threads", str(args.threads)]
+        log("configs %s: %s" % (",".join(group), " ".join(cmd[1:])))
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            raise SystemExit("bench: the config run %s failed with status %d" % (",".join(group), r.returncode))
+        out += [json.loads(l) for l in r.stdout.splitlines() if l.startswith("{")]
+    return out
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1, help="GPUs (one partition runs on one GPU: only 1)")
-    ap.add_argument("--steps", type=int, default=192, help="timed minibatches")
-    ap.add_argument("--warmup", type=int, default=8, help="untimed minibatches before them")
+    ap.add_argument("--steps", type=int, default=192, help="timed minibatches per window")
+    ap.add_argument("--warmup", type=int, default=8, help="untimed minibatches before the early window")
     ap.add_argument("--workload", default="cl111m_p64", help="a named synthetic workload (synth/workloads.py)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle baseline")
-    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baselines")
+    ap.add_argument("--no-configs", action="store_true", help="skip the smaller workloads")
+    ap.add_argument("--no-eviction-run", action="store_true", help="skip the eviction run and the sampler pass")
     ap.add_argument("--threads", type=int, default=None, help="host threads of the input generator")
     ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
     ap.add_argument("--depth", type=int, default=DEFAULT_DEPTH, help="batches in flight (1 to 3)")
     ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
     ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
     ap.add_argument("--buffer-pct", type=int, default=None, help="override f (percent of the halo)")
+    ap.add_argument("--headline-groups", default="all",
+                    help="kernel groups timed with HIP events in the headline window: 'all', or a comma list "
+                         "of sample_dedup,classify,gather_hbm,gather_miss,evict_round,refill")
+    ap.add_argument("--early-groups", default="all", help="kernel groups timed in the early window (as above)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="one plain 256 MiB device copy before warmup (reference for HBM byte counters)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
+                         "--copy-probe: the gather's HBM bytes over the headline window")
+    ap.add_argument("--config-run", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--sweep", action="store_true",
                     help="the paper's parameter grid (f in 15/25/35/50 %%, gamma in 0.95/0.995/0.9995, delta in "
                          "16..1024) on the same inputs, plus no buffer and one static run per f; one JSON line each")
@@ -280,13 +493,19 @@ def main():
     ap.add_argument("--compare-mode", choices=COMPARE_MODES, default=None,
                     help="run one mode of --compare in this process (used by --compare itself)")
     args = ap.parse_args()
-    if args.compare and args.compare_mode is None:
-        compare([a for a in sys.argv[1:]])
-        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (each partition's "
               "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
+    if args.config_run:
+        config_run(args.config_run.split(","), args)
+        return
+    if args.compare and args.compare_mode is None:
+        compare([a for a in sys.argv[1:]])
+        return
 
     import synth
 
@@ -306,41 +525,53 @@ def main():
         overlap(w, g, local, store, sched, args)
         return
 
-    res = run_context(w, g, local, store, sched, args.warmup, args.steps, args.log_steps, args.copy_probe,
-                      args.depth)
-    sm = summarize(w, res)
-    K, rb = args.steps, w.row_bytes
-    log("timed %d steps in %.3fs: %.1f minibatches/s, %d rounds, %d evicted" %
-        (K, res["elapsed"], sm["mbps"], res["rounds"], res["evicted"]))
-    log("host link per step: %.1f MB miss gather (%.1f MB of them hits on refilling slots, written through), "
-        "%.1f MB refill copied (%.1f MB evicted); %.1f GB/s over the link" %
-        (sm["host_bytes"] / 1e6, sm["pend_bytes"] / 1e6, sm["refill_bytes"] / 1e6, sm["evicted_bytes"] / 1e6,
-         sm["link_gbps"]))
-    phases, P = (res["tim_prof"], res["prof_steps"]) if res.get("tim_prof") else (res["tim"], K)
-    log("HIP-event timing: gather_hbm over the timed steps; every group over %d further steps:" % P)
-    for name, (ms, calls) in phases.items():
-        log("  %-13s %9.3f ms total, %5d launches, %.1f us avg" % (name, ms, calls, 1e3 * ms / max(calls, 1)))
-    log("gather_hbm %.0f B/launch, %.1f us, %.1f GB/s (%.1f%% of HBM); miss fetch %.1f GB/s; hit rate %.3f" %
-        (sm["g_bytes"], sm["g_avg_s"] * 1e6, sm["g_gbps"], 100 * sm["g_gbps"] / HBM_PEAK_GBPS, sm["m_gbps"],
-         sm["hit_rate"]))
+    K = args.steps
+    early, head = window_plan(args.warmup, K, w.delta)
+    def groups(spec):
+        return True if spec == "all" else [x for x in spec.split(",") if x]
+    hg = groups(args.headline_groups)
+    windows = [("early", early[0], early[1], groups(args.early_groups))]
+    if head != early:
+        windows.append(("headline", head[0], head[1], hg))
+    res = run_context(w, g, local, store, sched, windows, args.depth, args.log_steps, args.copy_probe)
+    hl = "headline" if head != early else "early"
+    sm = summarize(w, res, hl)
+    sm_early = summarize(w, res, "early")
+    evr = None
+    if not args.no_eviction_run:
+        n_ev = EVICTION_RUN_ROUNDS * w.delta + 1 if 2 * w.delta + K < 20000 else 2 * K
+        rev = run_context(w, g, local, store, sched, [("run", 0, n_ev, True)], args.depth, first_alone=False,
+                          sampler_steps=SAMPLER_STEPS)
+        evr = summarize(w, rev, "run")
+        st = rev["stats"][:n_ev]
+        evr["hit_rate_per_step"] = (st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)).round(4).tolist()
+        evr["from_init"] = True
+        evr["sampler"] = sampler_summary(rev, w)
 
-    copy_gbps = copy_reference(sm["g_bytes"])
-    log("plain device copy moving the same bytes (%d B): %.1f GB/s; the gather reaches %.1f%% of it" %
-        (round(sm["g_bytes"]), copy_gbps, 100 * sm["g_gbps"] / copy_gbps))
+    g_ = sm["gather_hbm"]
+    log("headline window steps %d..%d: %.1f minibatches/s, %d rounds, hit rate %.3f, bound %s %s" %
+        (head[0], head[1] - 1, sm["value"], sm["eviction_rounds"], sm["hit_rate"], sm["minibatch_roofline"]["bound"],
+         sm["minibatch_roofline"]["fractions"]))
+    log("gather_hbm %d B/launch, %.1f us, %.1f GB/s (%.1f%% of HBM)" % (g_["bytes_per_launch"], g_["avg_us"],
+                                                                       g_["GBps"], 100 * g_["frac_hbm"]))
+    copy_gbps = copy_reference(g_["bytes_per_launch"])
+    log("plain device copy moving the same bytes: %.1f GB/s; the gather reaches %.1f%% of it" %
+        (copy_gbps, 100 * g_["GBps"] / copy_gbps))
 
+    configs = None if args.no_configs else configs_in_children(args)
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(w, g, local, store, sched, args.cpu_seconds, res["first_steps"], res["state0"])
 
-    g_gbps = sm["g_gbps"]
+    traffic = gather_traffic(head, w.name)
     out = {
         "metric": "sampled+gathered minibatches/s; gather GB/s (% HBM peak); halo buffer hit rate",
-        "value": round(sm["mbps"], 3),
+        "value": sm["value"],
         "unit": "minibatches/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": round(1e3 * res["elapsed"] / K, 4),
+        "warmup": head[0],
+        "ms_per_step": sm["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -348,38 +579,91 @@ def main():
         "data": "synthetic (seeded Chung-Lu power-law graph, N(0,1) features)",
         "config": {"workload": w.name, "nodes": w.n, "partitions": w.parts, "partition": 0,
                    "L": g.L, "H": g.H, "csr_entries": g.nnz, "batch": w.batch, "fanout": list(w.fanout),
-                   "row_bytes": rb, "buffer_pct": w.buffer_pct, "gamma": w.gamma, "delta": w.delta,
-                   "cap": res["gm_cap"], "steps_timed": [args.warmup, args.warmup + K - 1],
-                   "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"], "lookahead": res["depth"] - 1,
+                   "row_bytes": w.row_bytes, "buffer_pct": w.buffer_pct, "gamma": w.gamma, "delta": w.delta,
+                   "cap": res["gm_cap"], "steps_timed": sm["steps_timed"],
+                   "eviction_rounds": sm["eviction_rounds"], "evicted_rows": sm["evicted_rows"],
+                   "refilled_rows": sm["refilled_rows"], "lookahead": res["depth"] - 1,
+                   "warmup_requested": args.warmup,
+                   "window_rule": "the timed steps lie after the first eviction round and contain a round "
+                                  "(centred on one when shorter than delta); the steps before them run untimed",
                    "parallelism": "one partition on one GPU"},
-        "gather_GBps": round(g_gbps, 1),
-        "gather_frac_hbm": round(g_gbps / HBM_PEAK_GBPS, 4),
-        "hit_rate": round(sm["hit_rate"], 4),
-        "roofline": {"bound": "hbm", "kernel": "gather_hbm", "achieved": round(g_gbps, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(g_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": gather_traffic(sm["g_bytes"]) if w.name == "cl111m_p64" else None,
-                     "bytes_per_launch": round(sm["g_bytes"]), "avg_us": round(sm["g_avg_s"] * 1e6, 2),
+        "gather_GBps": g_["GBps"],
+        "gather_frac_hbm": g_["frac_hbm"],
+        "hit_rate": sm["hit_rate"],
+        "roofline": {"bound": "hbm", "kernel": "gather_hbm", "achieved": g_["GBps"], "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": g_["frac_hbm"], "traffic": traffic,
+                     "traffic_from": None if traffic is None else
+                     "rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of the same command, averaged over the "
+                     "same window's launches, scaled by a plain copy's counters",
+                     "bytes_per_launch": g_["bytes_per_launch"], "avg_us": g_["avg_us"],
                      "plain_copy_same_bytes_GBps_events": round(copy_gbps, 1),
-                     "frac_of_plain_copy": round(sm["g_gbps"] / copy_gbps, 4)},
-        "host_link": {"kernel": "gather_miss", "achieved": round(sm["m_gbps"], 2), "peak": PCIE_PEAK_GBPS,
-                      "unit": "GB/s", "bytes_per_launch": round(sm["m_bytes"]),
-                      "avg_us": round(sm["m_avg_us"], 2),
-                      "refill_bytes_per_step": round(sm["refill_bytes"]),
-                      "link_GBps_whole_run": round(sm["link_gbps"], 2)},
-        "minibatch_roofline": {"bound": "host link",
-                               "hbm_alg_bytes_per_step": round(sm["b_alg"]),
-                               "hbm_GBps": round(sm["mbps"] * sm["b_alg"] / 1e9, 1),
-                               "hbm_frac": round(sm["mbps"] * sm["b_alg"] / 1e9 / HBM_PEAK_GBPS, 4),
-                               "link_bytes_per_step": round(sm["link_bytes"]),
-                               "link_GBps": round(sm["mbps"] * sm["link_bytes"] / 1e9, 2),
-                               "link_peak_GBps": PCIE_PEAK_GBPS,
-                               "link_frac": round(sm["mbps"] * sm["link_bytes"] / 1e9 / PCIE_PEAK_GBPS, 4)},
-        "phase_ms_per_step": {k: round(v[0] / P, 4) for k, v in phases.items()},
-        "phases_from": "%d steps after the timed region, every kernel group timed with HIP events" % P,
+                     "frac_of_plain_copy": round(g_["GBps"] / copy_gbps, 4)},
+        "host_link": dict(sm["gather_miss"] or {}, kernel="gather_miss", peak=PCIE_PEAK_GBPS, unit="GB/s",
+                          link_GBps_window=sm["minibatch_roofline"]["link_GBps"],
+                          refill_rows_per_step=sm["refill_rows_per_step"]),
+        "minibatch_roofline": sm["minibatch_roofline"],
+        "phase_ms_per_step": sm["phase_ms_per_step"],
+        "phases_from": "the timed window's own steps (HIP events on %s)" % sm["phases_timed"],
+        "early_window": {k: sm_early[k] for k in ("steps_timed", "eviction_rounds", "value", "ms_per_step",
+                                                  "hit_rate", "minibatch_roofline", "phase_ms_per_step",
+                                                  "host_rows_per_step", "refill_rows_per_step")},
+        "eviction_run": evr,
+        "configs": configs,
         "init_s": round(res["init_s"], 3),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def pmc_summary(args):
+    """Summary of two rocprofv3 counter runs of the default bench with
+    --copy-probe (FETCH_SIZE, then WRITE_SIZE): per k_gather_hbm dispatch of
+    the first context, the counters over the headline window's launches
+    (dispatch i of the gather is step i), each scaled by what the counter
+    reads for the plain 256 MiB copy of the probe (the last copy kernel before
+    step 0's first kernel). Prints the summary for profiles/."""
+    import csv
+    import hashlib
+    fetch_dir, write_dir = args.pmc_summary
+
+    def rows(d, counter):
+        path = [os.path.join(r, f) for r, _, fs in os.walk(d) for f in fs if f.endswith("counter_collection.csv")]
+        assert len(path) == 1, path
+        out = []
+        for r in csv.DictReader(open(path[0])):
+            if r["Counter_Name"] == counter:
+                out.append((int(r["Process_Id"]), int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+        out.sort(key=lambda x: (x[0], x[1]))
+        pid = out[0][0]
+        return [x for x in out if x[0] == pid]
+
+    import synth
+    K = args.steps
+    w = synth.get(args.workload)
+    _, head = window_plan(args.warmup, K, args.delta or w.delta)
+    res = {}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rs = rows(d, name)
+        first_step = next(i for i, x in enumerate(rs) if "k_seed_init" in x[2] or "k_row_scan" in x[2])
+        probe = [x for x in rs[:first_step] if "copyBuffer" in x[2]][-1]
+        gathers = [x[3] for x in rs if "k_gather_hbm" in x[2]]
+        res[name] = (probe[3], gathers)
+    probe_kib = 256 * 1024
+    f_scale = probe_kib / res["FETCH_SIZE"][0]
+    w_scale = probe_kib / res["WRITE_SIZE"][0]
+    fe = np.array(res["FETCH_SIZE"][1][head[0]:head[1]]) * f_scale * 1024
+    wr = np.array(res["WRITE_SIZE"][1][head[0]:head[1]]) * w_scale * 1024
+    src = open(os.path.join(ROOT, "paper_2410_22697_amd", "csrc", "buffer_kernels.hpp")).read()
+    a, b = src.find("// ---------------------------------------------------------------- gather"), src.find("// misses: pinned host store")
+    print("probe FETCH_SIZE %.1f KiB -> factor %.4f; WRITE_SIZE %.1f KiB -> factor %.4f" %
+          (res["FETCH_SIZE"][0], f_scale, res["WRITE_SIZE"][0], w_scale))
+    print("k_gather_hbm dispatches in the first context: %d; window %d..%d" % (len(res["FETCH_SIZE"][1]), head[0],
+                                                                              head[1] - 1))
+    print("HBM read per launch (scaled)  %.0f" % fe.mean())
+    print("HBM write per launch (scaled) %.0f" % wr.mean())
+    print("window_steps: %d..%d" % (head[0], head[1] - 1))
+    print("traffic_bytes_per_launch: %d" % round(fe.mean() + wr.mean()))
+    print("gather_source_sha256: %s" % hashlib.sha256(src[a:b].encode()).hexdigest())
 
 
 COMPARE_MODES = ("no_buffer", "static", "eviction")
@@ -399,23 +683,25 @@ def compare_one(w, name, g, local, store, sched, args):
     measurements of the JSON line, without the ratios to the no-buffer mode."""
     wm = compare_workload(w, name, args.warmup + args.steps)
     log("mode %s: f=%d%% delta=%d gamma=%g" % (name, wm.buffer_pct, wm.delta, wm.gamma))
-    res = run_context(wm, g, local, store, sched, args.warmup, args.steps)
-    sm = summarize(wm, res)
+    warm = max(1, args.warmup)
+    res = run_context(wm, g, local, store, sched, [("run", warm, warm + args.steps, ["gather_hbm"])])
+    sm = summarize(wm, res, "run")
     st = res["stats"]
     series = (st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)).round(4).tolist()  # per step, from step 0
     return {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": name,
-            "value": round(sm["mbps"], 3), "unit": "minibatches/s", "n_gpus": 1, "steps": args.steps,
-            "warmup": args.warmup, "dtype": "f32" if wm.dtype == "f32" else "bf16",
+            "value": sm["value"], "unit": "minibatches/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": warm, "dtype": "f32" if wm.dtype == "f32" else "bf16",
             "config": {"workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
-                       "cap": res["gm_cap"], "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"]},
+                       "cap": res["gm_cap"], "eviction_rounds": sm["eviction_rounds"],
+                       "evicted_rows": sm["evicted_rows"]},
             "init_s": round(res["init_s"], 3), "init_rows_over_link": res["gm_cap"],
-            "hit_rate": round(sm["hit_rate"], 4),
-            "halo_rows_per_step": round(sm["halo_rows"], 1),
-            "remote_rows_per_step": round(sm["remote_rows"], 1),
-            "miss_gather_rows_per_step": round(sm["host_bytes"] / wm.row_bytes, 1),
-            "refill_rows_per_step": round(sm["refill_bytes"] / wm.row_bytes, 1),
-            "link_GBps_whole_run": round(sm["link_gbps"], 2),
-            "gather_frac_hbm": round(sm["g_gbps"] / HBM_PEAK_GBPS, 4),
+            "hit_rate": sm["hit_rate"],
+            "halo_rows_per_step": sm["halo_rows_per_step"],
+            "remote_rows_per_step": sm["remote_rows_per_step"],
+            "miss_gather_rows_per_step": sm["host_rows_per_step"],
+            "refill_rows_per_step": sm["refill_rows_per_step"],
+            "link_GBps_window": sm["minibatch_roofline"]["link_GBps"],
+            "gather_frac_hbm": sm["gather_hbm"]["frac_hbm"] if sm["gather_hbm"] else None,
             "hit_rate_per_step": series}
 
 
@@ -425,8 +711,7 @@ def compare(argv):
     without eviction (the initial degree-ranked buffer kept for the whole run)
     and prefetch with eviction. Same graph, features and seed schedule; each
     mode in a process of its own, started from this one (which does not use
-    the GPU): with the three modes in one process, the third context was
-    measured 8-29% slower, whichever mode it was."""
+    the GPU)."""
     import subprocess
     outs = {}
     for name in COMPARE_MODES:
@@ -454,23 +739,26 @@ def sweep(w, g, local, store, sched, args):
     total = warm + steps
 
     def point(kind, wm, base):
-        res = run_context(wm, g, local, store, sched, warm, steps, timed_groups=True, prof_steps=0)
-        sm = summarize(wm, res)
+        res = run_context(wm, g, local, store, sched, [("run", warm, total, True)])
+        sm = summarize(wm, res, "run")
         st = res["stats"]
         hr = st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)
         win = [round(float(x.mean()), 4) for x in np.array_split(hr, max(1, total // 64))]
+        tim = res["windows"]["run"]["tim"]
         out = {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": kind,
                "workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
-               "steps": steps, "warmup": warm, "value": round(sm["mbps"], 3), "unit": "minibatches/s",
-               "hit_rate": round(sm["hit_rate"], 4), "eviction_rounds": res["rounds"], "evicted_rows": res["evicted"],
-               "remote_rows_per_step": round(sm["remote_rows"], 1),
-               "remote_rows_vs_no_buffer": round(sm["remote_rows"] / base["remote_rows"], 4) if base else 1.0,
-               "speedup_vs_no_buffer": round(sm["mbps"] / base["mbps"], 4) if base else 1.0,
-               "evict_ms_per_round": round(res["tim"]["evict_round"][0] / max(res["tim"]["evict_round"][1], 1), 3),
+               "steps": steps, "warmup": warm, "value": sm["value"], "unit": "minibatches/s",
+               "hit_rate": sm["hit_rate"], "eviction_rounds": sm["eviction_rounds"],
+               "evicted_rows": sm["evicted_rows"],
+               "remote_rows_per_step": sm["remote_rows_per_step"],
+               "remote_rows_vs_no_buffer": round(sm["remote_rows_per_step"] / base["remote_rows_per_step"], 4)
+               if base else 1.0,
+               "speedup_vs_no_buffer": round(sm["value"] / base["value"], 4) if base else 1.0,
+               "evict_ms_per_round": round(tim["evict_round"][0] / max(tim["evict_round"][1], 1), 3),
                "hit_rate_per_64_steps": win}
         log("%-9s f=%2d%% gamma=%-6g delta=%-5d %8.1f mb/s  hit %.3f  remote rows %.0f (%.3f)  rounds %d" %
-            (kind, wm.buffer_pct, wm.gamma, wm.delta, sm["mbps"], sm["hit_rate"], sm["remote_rows"],
-             out["remote_rows_vs_no_buffer"], res["rounds"]))
+            (kind, wm.buffer_pct, wm.gamma, wm.delta, sm["value"], sm["hit_rate"], sm["remote_rows_per_step"],
+             out["remote_rows_vs_no_buffer"], sm["eviction_rounds"]))
         print(json.dumps(out), flush=True)
         return sm
 
@@ -600,6 +888,8 @@ def overlap(w, g, local, store, sched, args):
     torch.cuda.synchronize()
     del bbs
     gm.close()
+
+
 
 
 def cpu_baseline(w, g, local, store, sched, budget_s, first_steps, state0=None):

@@ -194,11 +194,13 @@ int massive_info(const massive_ctx* ctx, int64_t* cap, float* alpha);
  * Each timed group adds event packets to its streams, so a run that must not
  * be slowed times only what it needs. MASSIVE_EINVAL for bits outside the
  * mask. */
-#define MASSIVE_TIMING_ALL 0x3F
+#define MASSIVE_TIMING_ALL 0x7F
 int massive_set_timing(massive_ctx* ctx, int groups);
 /* Totals since enabled: out_ms[i] summed milliseconds and out_calls[i]
  * launches for i = 0 sample+dedup, 1 classify, 2 gather_hbm, 3 gather_miss,
- * 4 eviction round, 5 refill. Synchronises the context's streams. */
+ * 4 eviction round, 5 refill, 6 the last hop's sampler kernel alone (a part
+ * of group 0). out_ms and out_calls have room for 7 entries each.
+ * Synchronises the context's streams. */
 int massive_get_timing(massive_ctx* ctx, double* out_ms, int64_t* out_calls);
 
 /* Frees every device and host resource of the context; NULL is a no-op.

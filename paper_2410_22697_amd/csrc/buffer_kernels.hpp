@@ -93,7 +93,8 @@ struct ClassifyArgs {
 };
 
 constexpr int kClsNT = 256;
-constexpr int kClsItems = 8;  // rows per thread: one block classifies 2048 rows
+constexpr int kClsItems = 2;  // rows per thread: one block classifies 512 rows per pass
+constexpr int kClsBlocks = 1024;  // grid bound: the blocks stride over the frontier the step found
 
 // Block-level aggregation: each block counts its rows per class, takes one
 // base per list with a single atomic, and places rows with wave ballots.

@@ -43,6 +43,7 @@ inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
 }  // namespace
 
 constexpr int kSlots = MASSIVE_MAX_INFLIGHT;
+constexpr int kTimingGroups = 7;  // bits of MASSIVE_TIMING_ALL
 
 struct massive_ctx {
   // configuration
@@ -143,8 +144,8 @@ struct massive_ctx {
   int timing = 0;  // bit g: group g is timed
   std::vector<hipEvent_t> ev_pool;
   std::vector<TimedRange> pending;
-  double tms[6] = {};
-  int64_t tcalls[6] = {};
+  double tms[kTimingGroups] = {};
+  int64_t tcalls[kTimingGroups] = {};
   std::string err;
 
   int fail(int code, const char* fmt, ...) {
@@ -636,6 +637,23 @@ int massive_output_bounds(const massive_ctx* c, int32_t n_seeds, int64_t* n_boun
   return MASSIVE_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Per-step buffers of one enqueued step: those of the context's step slot,
+// or the no-alloc scratch array (then its scan flags are cleared per call,
+// fill kernels clear it, and nothing is timed).
+struct StepBufs {
+  ms::StepSizes* sz;
+  int2* hbm_list;
+  int2* miss_list;
+  int32_t* miss_slot;
+  int32_t* big;
+  uint64_t* flags;
+  bool from_scratch;
+};
+
 // The epoch of the next single-pass scan (flags of earlier epochs are stale
 // by their tag); the flags are cleared before the tags could wrap around.
 uint32_t next_scan_epoch(massive_ctx* c, hipStream_t s) {
@@ -646,18 +664,15 @@ uint32_t next_scan_epoch(massive_ctx* c, hipStream_t s) {
   return ++c->scan_epoch;
 }
 
-int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
-  if (!c) return MASSIVE_EINVAL;
+// Argument checks shared by the entry points that enqueue a step; nb and eb
+// receive the output bounds of the batch.
+int check_step_args(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io, int64_t* nb, int64_t* eb) {
   if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier failure");
   if (!io || n0 < 0 || (n0 > 0 && !seeds)) return c->fail(MASSIVE_EINVAL, "bad seeds / batch arguments");
   if (c->pending_round) return c->fail(MASSIVE_ESTATE, "massive_evict_step was not called after the last step");
   if (n0 > c->L) return c->fail(MASSIVE_EINVAL, "more seeds than local nodes");
-  const int slot = (int)(c->t % kSlots);
-  if (c->infl[slot].io)
-    return c->fail(MASSIVE_ESTATE, "%d batches in flight: wait for the oldest one first", kSlots);
   for (int i = 0; i < kSlots; ++i)
     if (c->infl[i].io == io) return c->fail(MASSIVE_ESTATE, "this batch is still in flight");
-  int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
   massive_output_bounds(c, n0, nb, eb);
   if (!io->nodes || !io->mask || !io->feat) return c->fail(MASSIVE_EINVAL, "nodes / mask / feat are NULL");
   if (io->nodes_cap < nb[c->K]) return c->fail(MASSIVE_ECAPACITY, "nodes_cap %lld < bound %lld",
@@ -683,14 +698,33 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       if (!device_visible(ptrs[i])) return c->fail(MASSIVE_EINVAL, "argument %d is not HIP-visible memory", i);
   }
 
+  return MASSIVE_OK;
+}
+
+// Enqueues one step (sampling and classify on the main stream, the gathers
+// and the step's completion on the side stream) with the per-step buffers sb.
+int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io, const int64_t* nb,
+                 const int64_t* eb, const StepBufs& sb) {
   hipStream_t s = c->s_main;
-  ms::StepSizes* sz = c->d_sz + slot;
-  int2* miss_list = c->d_miss_list[slot];
+  const int slot = (int)(c->t % kSlots);
+  ms::StepSizes* sz = sb.sz;
+  int2* miss_list = sb.miss_list;
   const uint32_t key0 = (uint32_t)c->seed, key1 = (uint32_t)(c->seed >> 32);
   // this slot's sizes and lists were last used by the side stream kSlots
   // steps ago (complete: that batch was waited for)
   CK(hipStreamWaitEvent(s, c->ev_batch_done[slot], 0));
-  CK(hipMemsetAsync(sz, 0, sizeof(ms::StepSizes), s));
+  // the scratch array may be shared with other contexts on this device: its
+  // scan flags are cleared here (any epoch from 1 on is then fresh), and it is
+  // cleared by fill kernels (nothing that a captured graph would replay wrongly)
+  uint32_t scratch_epoch = 0;
+  auto epoch = [&]() { return sb.from_scratch ? ++scratch_epoch : next_scan_epoch(c, s); };
+  if (sb.from_scratch) {
+    ms::k_fill<int32_t><<<1, 256, 0, s>>>(reinterpret_cast<int32_t*>(sz), (int64_t)(sizeof(ms::StepSizes) / 4), 0);
+    const int64_t words = std::max(cdiv(nb[c->K], ms::kScanTile), cdiv(c->W, ms::kScanTile)) + 1;
+    ms::k_fill<uint64_t><<<grid_for(words, 256, 64), 256, 0, s>>>(sb.flags, words, 0ull);
+  } else {
+    CK(hipMemsetAsync(sz, 0, sizeof(ms::StepSizes), s));
+  }
   {
     massive_ctx::Range tr(c, s, 0);
     if (n0 > 0)
@@ -701,8 +735,8 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       // the previous hop's relabel shares the launch
       const int64_t nrel = k > 1 ? (int64_t)grid_for(eb[k - 2], ms::kScanTile, 1024) : 0;
       ms::k_row_scan<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
-          c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], c->d_scan_flags, next_scan_epoch(c, s),
-          c->d_big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
+          c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], sb.flags, epoch(),
+          sb.big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;
@@ -718,26 +752,36 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
       sa.err = &sz->status;
       sa.mu32 = c->mu32[k - 1];
       sa.big_min = c->big_min;
-      sa.big_rows = c->d_big;
+      sa.big_rows = sb.big;
       sa.pos_of = c->d_pos_of;
       sa.bits = c->d_bits;
       sa.tau_iters = c->tau_iters;
       // a small frontier is bound by its longest rows: a block each; a large
-      // one keeps the chip busy: a wave each, longest first
+      // one keeps the chip busy: a wave each, longest first. The last hop's
+      // dispatch can carry its own start/stop events (timing group 6).
+      hipEvent_t hop_a = nullptr, hop_b = nullptr;
+      const bool timed = k == c->K && c->kernel_pair(6, &hop_a, &hop_b);
       if (nprev <= ms::kBlockRowsMax) {
         sa.row_waves = 0;
         sa.big_blocks = std::max<int64_t>(1, std::min<int64_t>(nprev, c->big_blocks));
-        ms::k_sample_blocks<<<(unsigned)(sa.big_blocks + std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves))),
-                              ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
+        const dim3 grid((unsigned)(sa.big_blocks + std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves))));
+        if (timed)
+          hipExtLaunchKernelGGL(ms::k_sample_blocks, grid, dim3(ms::kSampleWaves * MS_WAVE), 0, s, hop_a, hop_b, 0, sa);
+        else
+          ms::k_sample_blocks<<<grid, ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
       } else {
         sa.row_waves = nprev;  // the big list never exceeds the frontier
         sa.big_blocks = 0;
-        ms::k_sample_waves<<<(unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)),
-                             ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
+        const dim3 grid((unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)));
+        if (timed)
+          hipExtLaunchKernelGGL(ms::k_sample_waves, grid, dim3(ms::kSampleWaves * MS_WAVE), 0, s, hop_a, hop_b, 0, sa);
+        else
+          ms::k_sample_waves<<<grid, ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
       }
+      if (timed) c->pending.push_back({hop_a, hop_b, 6});
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_scan<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, c->d_scan_flags,
-                                                             next_scan_epoch(c, s), io->nodes, c->d_pos_of);
+      ms::k_bits_scan<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, sb.flags,
+                                                             epoch(), io->nodes, c->d_pos_of);
       if (k == c->K)
         ms::k_relabel<<<grid_for(eb[k - 1], ms::kScanTile, 1024), ms::kScanNT, 0, s>>>(io->indices[k - 1], sz, k,
                                                                                      c->d_pos_of);
@@ -776,13 +820,16 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     ca.rank_of = c->d_rank_of;
     ca.pos_of = c->d_pos_of;
     ca.mask = io->mask;
-    ca.hbm_list = c->d_hbm_list[slot];
+    ca.hbm_list = sb.hbm_list;
     ca.miss_list = miss_list;
-    ca.miss_slot = c->d_miss_slot[slot];
+    ca.miss_slot = sb.miss_slot;
     ca.slot_round = c->d_slot_round;
     ca.landed = c->d_landed;
     ca.pend_round = pend;
-    ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, 4096), ms::kClsNT, 0, s>>>(ca);
+    // the frontier's size is known on the device only: at most kClsBlocks
+    // blocks stride over it (a frontier far below the bound leaves the blocks
+    // past its end idle, not a long tail of dispatches)
+    ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, ms::kClsBlocks), ms::kClsNT, 0, s>>>(ca);
   }
   if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of, sz);
   CK(hipEventRecord(c->ev_cls_done[slot], s));
@@ -794,7 +841,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   hipStream_t sm = c->s_miss;
   CK(hipStreamWaitEvent(sm, c->ev_cls_done[slot], 0));
   if (c->refill_inflight) CK(hipStreamWaitEvent(sm, c->ev_refill_done, 0));
-  launch_gather(c, 2, kHbm, sm, c->d_hbm_list[slot], &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
+  launch_gather(c, 2, kHbm, sm, sb.hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
                 c->hbm_blocks);
   CK(hipEventRecord(c->ev_hbm_done[slot], sm));
   {
@@ -803,7 +850,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   }
   if (c->H > 0) {
     launch_gather(c, 3, kMiss, sm, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
-                  c->host_blocks, c->d_miss_slot[slot], c->d_slab + (int64_t)c->L * c->rb);
+                  c->host_blocks, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb);
   }
   CK(hipEventRecord(c->ev_miss_done[slot], sm));
   // rows written through into their slots are landed from here on; the
@@ -811,7 +858,7 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   {
     const bool publish = pend >= 0 && c->H > 0;
     ms::k_step_done<<<publish ? grid_for(nb[c->K], 256, 1024) : 1, 256, 0, sm>>>(
-        c->d_miss_slot[slot], &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, &c->d_ctr->bad,
+        sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, &c->d_ctr->bad,
         c->hd_sz + slot, c->hd_bad + slot);
   }
   CK(hipEventRecord(c->ev_batch_done[slot], sm));
@@ -823,6 +870,23 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
   c->t += 1;
   c->pending_round = true;
   return MASSIVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
+  if (!c) return MASSIVE_EINVAL;
+  int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
+  int rc = check_step_args(c, seeds, n0, io, nb, eb);
+  if (rc != MASSIVE_OK) return rc;
+  const int slot = (int)(c->t % kSlots);
+  if (c->infl[slot].io)
+    return c->fail(MASSIVE_ESTATE, "%d batches in flight: wait for the oldest one first", kSlots);
+  const StepBufs sb{c->d_sz + slot, c->d_hbm_list[slot], c->d_miss_list[slot], c->d_miss_slot[slot], c->d_big,
+                    c->d_scan_flags, false};
+  return enqueue_step(c, seeds, n0, io, nb, eb, sb);
 }
 
 int massive_batch_wait(massive_ctx* c, massive_batch* io) {
@@ -1049,7 +1113,7 @@ int massive_set_timing(massive_ctx* c, int groups) {
   CK(hipDeviceSynchronize());
   c->resolve_timing();
   c->timing = groups;
-  for (int i = 0; i < 6; ++i) {
+  for (int i = 0; i < kTimingGroups; ++i) {
     c->tms[i] = 0.0;
     c->tcalls[i] = 0;
   }
@@ -1062,7 +1126,7 @@ int massive_get_timing(massive_ctx* c, double* out_ms, int64_t* out_calls) {
   CK(hipStreamSynchronize(c->s_miss));
   CK(hipStreamSynchronize(c->s_copy));
   c->resolve_timing();
-  for (int i = 0; i < 6; ++i) {
+  for (int i = 0; i < kTimingGroups; ++i) {
     if (out_ms) out_ms[i] = c->tms[i];
     if (out_calls) out_calls[i] = c->tcalls[i];
   }

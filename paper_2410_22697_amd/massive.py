@@ -112,8 +112,9 @@ def _seed_count(seeds) -> int:
     return int(seeds.numel())
 
 
-TIMING_GROUPS = ("sample_dedup", "classify", "gather_hbm", "gather_miss", "evict_round", "refill")
-TIMING_ALL = 0x3F
+TIMING_GROUPS = ("sample_dedup", "classify", "gather_hbm", "gather_miss", "evict_round", "refill",
+                 "sample_last_hop")
+TIMING_ALL = 0x7F
 
 
 @dataclass
@@ -309,7 +310,7 @@ class Massive:
         self._check(self._lib.massive_set_timing(self._h, mask))
 
     def timing(self):
-        ms = np.zeros(6, np.float64)
-        calls = np.zeros(6, np.int64)
+        ms = np.zeros(len(TIMING_GROUPS), np.float64)
+        calls = np.zeros(len(TIMING_GROUPS), np.int64)
         self._check(self._lib.massive_get_timing(self._h, ms.ctypes.data, calls.ctypes.data))
         return {g: (float(ms[i]), int(calls[i])) for i, g in enumerate(TIMING_GROUPS)}

@@ -24,3 +24,25 @@ def test_help_lists_the_driver_flags():
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup"):
         assert flag in r.stdout
+
+
+def test_headline_window_holds_a_round_after_the_first():
+    """The headline window lies after the first eviction round (t = delta), so
+    refill traffic is in its steady state, contains a round (a step t > 0
+    with t mod delta = 0), and does not overlap the early window."""
+    sys.path.insert(0, ROOT)
+    from bench import window_plan
+    for delta in (1, 2, 3, 4, 8, 16, 32, 64, 100):
+        for steps in (1, 2, 5, 19, 20, 31, 32, 33, 64, 192):
+            for warmup in (0, 1, 5, 8, 50, 200):
+                early, head = window_plan(warmup, steps, delta)
+                assert early == (max(1, warmup), max(1, warmup) + steps)
+                a, b = head
+                assert b - a == steps
+                assert a > delta, (delta, steps, warmup, head)
+                assert any(t % delta == 0 for t in range(a, b)), (delta, steps, warmup, head)
+                assert a >= early[1]
+    # an interval too long for a round: the early window only
+    assert window_plan(5, 20, 100000) == ((5, 25), (5, 25))
+    # the driver's usual call: centred on the round at 2 delta
+    assert window_plan(5, 20, 32)[1] == (54, 74)

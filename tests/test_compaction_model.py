@@ -4,7 +4,7 @@ Algorithm 2 written as two gather lists). Per item of a block of 256 threads
 block's first thread takes one base per list from a global counter (blocks
 in any order); a wave's offset is the base plus the counts of the waves
 before it, and a lane's slot adds the matching lanes below it. Rows of one
-thread are items 0..7 at positions b0 + it * 256 + thread.
+thread are items 0..ITEMS-1 at positions b0 + it * 256 + thread.
 
 The model restates those steps, with blocks taking their bases in a random
 order, and checks that each list holds every row of its class exactly once
@@ -16,7 +16,7 @@ import random
 
 import pytest
 
-NT, WAVE, ITEMS = 256, 64, 8
+NT, WAVE, ITEMS = 256, 64, 2
 TILE = NT * ITEMS
 
 
@@ -68,7 +68,7 @@ def compact(cls, rnd):
     return hbm[:counters[0]], host[:counters[1]], counters
 
 
-@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 2047, 2048, 2049, 5000])
+@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 511, 512, 513, 2047, 2048, 2049, 5000])
 def test_every_row_lands_once_in_its_list(n):
     rnd = random.Random(n)
     for mix in ((0.3, 0.3, 0.3), (1.0, 0.0, 0.0), (0.0, 0.0, 1.0), (0.2, 0.5, 0.2)):

@@ -157,6 +157,7 @@ def test_timing_groups():
     gm.evict_step()
     tim = gm.timing()
     assert tim["sample_dedup"][1] == 1 and tim["gather_hbm"][1] == 1 and tim["gather_miss"][1] == 1
+    assert tim["sample_last_hop"][1] == 1 and 0 < tim["sample_last_hop"][0] <= tim["sample_dedup"][0]
     with pytest.raises(MassiveError) as ei:
         gm._check(gm._lib.massive_set_timing(gm._h, 1 << len(TIMING_GROUPS)))
     assert ei.value.code == -1
