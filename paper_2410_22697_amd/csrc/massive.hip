@@ -685,18 +685,14 @@ int check_step_args(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_ba
     if (eb[k] >= (1ll << 31)) return c->fail(MASSIVE_EINVAL, "hop %d may emit 2^31 edges or more", k + 1);
   }
   if (c->t >= 0xFFFFFFFFll) return c->fail(MASSIVE_ESTATE, "step counter exhausted");
-  {
-    // every pointer the kernels dereference must be visible to the device
-    const void* ptrs[3 + 2 * MASSIVE_MAX_HOPS] = {io->nodes, io->mask, io->feat};
-    int np = 3;
-    if (n0 > 0) ptrs[np++] = seeds;
-    for (int k = 0; k < c->K; ++k) {
-      ptrs[np++] = io->indptr[k];
-      ptrs[np++] = io->indices[k];
-    }
-    for (int i = 0; i < np; ++i)
-      if (!device_visible(ptrs[i])) return c->fail(MASSIVE_EINVAL, "argument %d is not HIP-visible memory", i);
-  }
+  // every pointer the kernels dereference must be visible to the device:
+  // nodes, mask, feat, the seeds and two arrays per hop (K <= MASSIVE_MAX_HOPS)
+  if (!device_visible(io->nodes) || !device_visible(io->mask) || !device_visible(io->feat))
+    return c->fail(MASSIVE_EINVAL, "nodes / mask / feat are not HIP-visible memory");
+  if (n0 > 0 && !device_visible(seeds)) return c->fail(MASSIVE_EINVAL, "seeds are not HIP-visible memory");
+  for (int k = 0; k < c->K; ++k)
+    if (!device_visible(io->indptr[k]) || !device_visible(io->indices[k]))
+      return c->fail(MASSIVE_EINVAL, "hop %d buffers are not HIP-visible memory", k + 1);
 
   return MASSIVE_OK;
 }
