@@ -132,6 +132,18 @@ typedef struct {
  * MASSIVE_EINVAL (no state change) if a seed is out of [0, L) or repeated. */
 int massive_sample(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
 
+/* massive_sample for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same step and the same results, but its per-step scratch (sizes, gather
+ * lists, scan flags) lives in one static device array per GPU, of fixed size,
+ * instead of the context's per-slot buffers, and the call itself allocates
+ * nothing (no hipMalloc, no event creation; timing is off for it). Limit:
+ * frontier bound n_bound[K] <= 1,310,720 rows; a larger bound is refused with
+ * MASSIVE_ECAPACITY. Synchronous, and refused (MASSIVE_ESTATE) while a batch
+ * of this context is in flight. Calls that overlap on one GPU, from any
+ * contexts, race on that array: serialise them. */
+int massive_sample_noalloc(massive_ctx* ctx, const int32_t* seeds, int32_t n_seeds, massive_batch* io);
+
 /* The asynchronous form of massive_sample, for look-ahead (Algorithm 1
  * prepares the next minibatch while the current one is consumed): enqueues
  * the step and returns at once. The batch's buffers must not be read or

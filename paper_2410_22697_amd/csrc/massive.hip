@@ -17,6 +17,7 @@
 #include <cstdlib>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -40,6 +41,41 @@ inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
   return (unsigned)std::min<int64_t>(std::max<int64_t>(g, 1), cap);
 }
 
+}  // namespace
+
+// ------------------------------------------------------------- no-alloc path
+// massive_sample_noalloc takes a step's per-step buffers (sizes, the two
+// gather lists, the write-through slots, the big-row list, the scan flags)
+// from this file-scope array instead of the context's. Layout: StepSizes
+// (256 B) | hbm list int2[kNoAllocMaxRows] | miss list int2[..] | write-through
+// slots int32[..] | big rows int32[..] | scan flags uint64[kNoAllocFlagWords].
+// Each GPU holds its own copy (~30 MiB) while the library is loaded; its device
+// address is looked up once per device, in massive_init.
+constexpr int64_t kNoAllocMaxRows = 1310720;  // frontier rows (covers a 1,081,344-row bound)
+constexpr int64_t kNoAllocFlagWords = (int64_t(1) << 31) / 32 / ms::kScanTile + 2;  // any L + H < 2^31
+constexpr int64_t kNoAllocBytes = 256 + kNoAllocMaxRows * (8 + 8 + 4 + 4) + kNoAllocFlagWords * 8;
+static_assert(sizeof(ms::StepSizes) <= 256, "sizes fit the first 256 bytes");
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};  // device address of `scratch` on each device, once looked up
+
+// The device address of `scratch` on device dev, which must be current: the
+// array's name in host code is a host-side stand-in, not a device address.
+hipError_t scratch_address(int dev, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev] = ptr;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
 }  // namespace
 
 constexpr int kSlots = MASSIVE_MAX_INFLIGHT;
@@ -134,6 +170,8 @@ struct massive_ctx {
   bool pending_round = false;
   bool broken = false;
   int64_t failed_step = -1;  // earliest step whose batch failed on the device (-1: none)
+  int device = -1;            // the device current at init (its streams and memory)
+  uint8_t* d_scratch = nullptr;  // device address of the no-alloc scratch array on that device
   struct InFlight {
     massive_batch* io = nullptr;
     int64_t step = -1;
@@ -453,6 +491,13 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (const char* e = getenv("MASSIVE_BIG_BLOCKS")) c->big_blocks = std::max<int64_t>(1, atoll(e));
   if (const char* e = getenv("MASSIVE_TAU_ITERS")) c->tau_iters = std::min(std::max(0, atoi(e)), ms::kTauIters);
   c->s_main = (hipStream_t)a->stream;
+  CK(hipGetDevice(&c->device));
+  if (c->device < 0 || c->device >= kMaxDevices) return c->fail(MASSIVE_EHIP, "device %d out of range", c->device);
+  {
+    void* p = nullptr;
+    CK(scratch_address(c->device, &p));
+    c->d_scratch = static_cast<uint8_t*>(p);
+  }
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
   for (int i = 0; i < kSlots; ++i)
@@ -949,6 +994,40 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
 
 int massive_sample(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
   int rc = massive_sample_async(c, seeds, n0, io);
+  if (rc != MASSIVE_OK) return rc;
+  return massive_batch_wait(c, io);
+}
+
+int massive_sample_noalloc(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch* io) {
+  if (!c) return MASSIVE_EINVAL;
+  int64_t nb[MASSIVE_MAX_HOPS + 1], eb[MASSIVE_MAX_HOPS];
+  int rc = check_step_args(c, seeds, n0, io, nb, eb);
+  if (rc != MASSIVE_OK) return rc;
+  for (int i = 0; i < kSlots; ++i)
+    if (c->infl[i].io) return c->fail(MASSIVE_ESTATE, "a batch is in flight: wait for it before a no-alloc step");
+  if (nb[c->K] > kNoAllocMaxRows)
+    return c->fail(MASSIVE_ECAPACITY, "the no-alloc scratch holds %lld frontier rows, this batch's bound is %lld "
+                                      "(massive_sample has no such limit)",
+                   (long long)kNoAllocMaxRows, (long long)nb[c->K]);
+  const int64_t words = std::max(cdiv(nb[c->K], ms::kScanTile), cdiv(c->W, ms::kScanTile)) + 1;
+  if (words > kNoAllocFlagWords)
+    return c->fail(MASSIVE_ECAPACITY, "the no-alloc scratch holds %lld scan flags, this step needs %lld",
+                   (long long)kNoAllocFlagWords, (long long)words);
+  if (!c->d_scratch) return c->fail(MASSIVE_EHIP, "the no-alloc scratch has no device address");
+  uint8_t* base = c->d_scratch;
+  StepBufs sb;
+  sb.sz = reinterpret_cast<ms::StepSizes*>(base);
+  sb.hbm_list = reinterpret_cast<int2*>(base + 256);
+  sb.miss_list = sb.hbm_list + kNoAllocMaxRows;
+  sb.miss_slot = reinterpret_cast<int32_t*>(sb.miss_list + kNoAllocMaxRows);
+  sb.big = sb.miss_slot + kNoAllocMaxRows;
+  sb.flags = reinterpret_cast<uint64_t*>(sb.big + kNoAllocMaxRows);
+  sb.from_scratch = true;
+  // timing events are created on demand: this path records none
+  const int timing = c->timing;
+  c->timing = 0;
+  rc = enqueue_step(c, seeds, n0, io, nb, eb, sb);
+  c->timing = timing;
   if (rc != MASSIVE_OK) return rc;
   return massive_batch_wait(c, io);
 }

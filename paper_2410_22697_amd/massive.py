@@ -19,7 +19,7 @@ OK, EINVAL, ECAPACITY, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
 MAX_INFLIGHT = 3  # batches enqueued with sample_async and not yet waited for
 _NAMES = {EINVAL: "EINVAL", ECAPACITY: "ECAPACITY", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE"}
 
-EXPORTS = ("massive_init", "massive_output_bounds", "massive_sample", "massive_sample_async",
+EXPORTS = ("massive_init", "massive_output_bounds", "massive_sample", "massive_sample_noalloc", "massive_sample_async",
            "massive_batch_wait", "massive_evict_step", "massive_get_counters", "massive_get_state",
            "massive_get_buffer_rows", "massive_info", "massive_set_timing", "massive_get_timing",
            "massive_destroy", "massive_last_error")
@@ -69,6 +69,7 @@ def load():
     lib.massive_init.argtypes = [P(InitArgs), P(vp)]
     lib.massive_output_bounds.argtypes = [vp, i32, vp, vp]
     lib.massive_sample.argtypes = [vp, vp, i32, P(Batch)]
+    lib.massive_sample_noalloc.argtypes = [vp, vp, i32, P(Batch)]
     lib.massive_sample_async.argtypes = [vp, vp, i32, P(Batch)]
     lib.massive_batch_wait.argtypes = [vp, P(Batch)]
     lib.massive_evict_step.argtypes = [vp, vp, vp, vp, vp]
@@ -241,6 +242,16 @@ class Massive:
         n0 = _seed_count(seeds)
         self._check(self._lib.massive_sample(self._h, seeds.data_ptr() if n0 else None, n0,
                                              ctypes.byref(bb.c)))
+        c = bb.c
+        return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
+                          local=int(c.local), hits=int(c.hits), misses=int(c.misses), host_rows=int(c.host_rows))
+
+    def sample_noalloc(self, seeds, bb: BatchBuffers) -> StepResult:
+        """massive_sample with its per-step scratch in the library's static
+        device array (the call allocates nothing); synchronous."""
+        n0 = _seed_count(seeds)
+        self._check(self._lib.massive_sample_noalloc(self._h, seeds.data_ptr() if n0 else None, n0,
+                                                     ctypes.byref(bb.c)))
         c = bb.c
         return StepResult(n=[int(c.n[k]) for k in range(self.K + 1)], e=[int(c.e[k]) for k in range(self.K)],
                           local=int(c.local), hits=int(c.hits), misses=int(c.misses), host_rows=int(c.host_rows))
