@@ -93,21 +93,26 @@ struct ClassifyArgs {
 };
 
 constexpr int kClsNT = 256;
-constexpr int kClsItems = 2;  // rows per thread: one block classifies 512 rows per pass
-constexpr int kClsBlocks = 1024;  // grid bound: the blocks stride over the frontier the step found
+constexpr int kClsItems = 4;  // rows per thread: one block classifies 1024 rows per pass
+constexpr int kClsBlocks = 512;  // grid bound: the blocks stride over the frontier the step found
 
-// Block-level aggregation: each block counts its rows per class, takes one
-// base per list with a single atomic, and places rows with wave ballots.
-// The loads of a thread go out in three rounds, each for all its rows: the
+// Block-level aggregation: each block counts its rows per list, takes one
+// base per list with a single atomic, and places rows with wave ballots. The
+// step's local, hit and miss counts need no atomics here: the local rows are
+// the seeds plus the new nodes below L that the dedup scans counted, and the
+// completion kernel derives hits and misses from the two list lengths (and
+// the hits on slots still refilling, counted here only while a refill is in
+// flight). Hits add one to their slot's count with a no-return atomic.
+// The loads of a thread go out in rounds, each for all its rows: the
 // frontier ids; a window of four table entries from each id's probe start
 // (the 16-byte pairs holding entries p & ~1 .. (p & ~1) + 3, which settle
-// almost every search; the rare rest probes on one by one); the hit slots'
-// counters and refill stamps (and the misses' ranks: S_A is kept by rank).
-// Lanes past the end and local rows load dummy (in-range) addresses and
-// change nothing.
+// almost every search; the rare rest probes on one by one); the misses'
+// ranks (S_A is kept by rank) and, while a refill is in flight, the hit
+// slots' refill stamps. Lanes past the end and local rows load dummy
+// (in-range) addresses and change nothing.
 __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   constexpr int NW = kClsNT / MS_WAVE;
-  __shared__ int32_t wc[NW][4];          // per-wave counts: hbm list, host list, local, pending hits
+  __shared__ int32_t wc[NW][3];          // per-wave counts: hbm list, host list, pending hits
   __shared__ unsigned long long base[2];
   if (a.sz->status) return;
   const int64_t n = a.sz->n[a.K];
@@ -155,11 +160,10 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
         slot[it] = r;
       }
     }
-    int32_t hc[kClsItems], sr[kClsItems], ld[kClsItems], rk[kClsItems];
+    int32_t sr[kClsItems], ld[kClsItems], rk[kClsItems];
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
       const int32_t sl = slot[it] >= 0 ? slot[it] : 0;
-      hc[it] = a.hitcnt[sl];
       rk[it] = a.rank_of[v[it] >= a.L && slot[it] < 0 ? v[it] - a.L : 0];
       sr[it] = 0;
       ld[it] = 0;
@@ -170,14 +174,13 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
     }
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
-      pin(hc[it]);
       pin(sr[it]);
       pin(ld[it]);
       pin(rk[it]);
     }
     int cls[kClsItems];
     int32_t src[kClsItems], wslot[kClsItems];
-    int ch = 0, cm = 0, cl = 0, cp = 0;  // hbm list, host list, local, pending hits
+    int ch = 0, cm = 0, cp = 0;  // hbm list, host list, pending hits
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
       const int64_t i = b0 + (int64_t)it * kClsNT + threadIdx.x;
@@ -193,7 +196,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
         } else if (slot[it] >= 0) {
           cls[it] = 1;
           src[it] = a.L + slot[it];
-          a.hitcnt[slot[it]] = hc[it] + 1;
+          atomicAdd(&a.hitcnt[slot[it]], 1);  // each slot once per step: no contention
           // a hit on a slot whose refill may not have landed reads the same
           // row from the host store
           if (pending && sr[it] == a.pend_round && ld[it] != a.pend_round) {
@@ -210,29 +213,24 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
       }
       ch += __popcll(ballot(cls[it] == 0 || cls[it] == 1));
       cm += __popcll(ballot(cls[it] >= 2));
-      cl += __popcll(ballot(cls[it] == 0));
-      cp += __popcll(ballot(cls[it] == 3));
+      if (pending) cp += __popcll(ballot(cls[it] == 3));
     }
     if (lane == 0) {
       wc[wave][0] = ch;
       wc[wave][1] = cm;
-      wc[wave][2] = cl;
-      wc[wave][3] = cp;
+      wc[wave][2] = cp;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-      int th = 0, tm = 0, tl = 0, tp = 0;
+      int th = 0, tm = 0, tp = 0;
       for (int w = 0; w < NW; ++w) {
         th += wc[w][0];
         tm += wc[w][1];
-        tl += wc[w][2];
-        tp += wc[w][3];
+        tp += wc[w][2];
       }
       base[0] = th ? atomicAdd((unsigned long long*)&a.sz->n_hbm, (unsigned long long)th) : 0ull;
       base[1] = tm ? atomicAdd((unsigned long long*)&a.sz->n_miss, (unsigned long long)tm) : 0ull;
-      if (tl) atomicAdd((unsigned long long*)&a.sz->local, (unsigned long long)tl);
-      if (th - tl + tp) atomicAdd((unsigned long long*)&a.sz->hits, (unsigned long long)(th - tl + tp));
-      if (tm - tp) atomicAdd((unsigned long long*)&a.sz->misses, (unsigned long long)(tm - tp));
+      if (tp) atomicAdd((unsigned long long*)&a.sz->n_pending, (unsigned long long)tp);
     }
     __syncthreads();
     // this wave's offset inside the block's share of each list
@@ -364,14 +362,17 @@ __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ li
 
 // The step's last kernel, after k_gather_miss (a kernel boundary: its row
 // writes are complete): the written-through slots are landed for round
-// `round_id` (none if round_id < 0), and block 0 copies the step's sizes and
-// the eviction-round consistency flag into the pinned host mailbox (device
-// view), made visible to the host before the kernel ends.
+// `round_id` (none if round_id < 0), and block 0 derives the step's counts
+// (local rows: the seeds plus the new nodes below L of each hop; hits: the
+// HBM list's buffer rows plus the hits read over the host link; misses: the
+// rest of the host list), then copies the step's sizes and the eviction-round
+// consistency flag into the pinned host mailbox (device view), made visible
+// to the host before the kernel ends.
 constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
 static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
 __global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ wslot,
                                                    const int64_t* __restrict__ count, int32_t* __restrict__ landed,
-                                                   int64_t cap, int32_t round_id, const StepSizes* __restrict__ sz,
+                                                   int64_t cap, int32_t round_id, StepSizes* __restrict__ sz, int32_t K,
                                                    const int32_t* __restrict__ bad, StepSizes* h_sz, int32_t* h_bad) {
   if (round_id >= 0) {
     const int64_t n = *count;
@@ -382,6 +383,14 @@ __global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ w
   }
   if (blockIdx.x == 0) {
     const int i = threadIdx.x;
+    if (i == 0 && !sz->status) {
+      int64_t local = sz->n[0];
+      for (int k = 0; k < K; ++k) local += sz->n_local_new[k];
+      sz->local = local;
+      sz->hits = sz->n_hbm - local + sz->n_pending;
+      sz->misses = sz->n_miss - sz->n_pending;
+    }
+    __syncthreads();
     if (i < kSizeWords) reinterpret_cast<int32_t*>(h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
     if (i == kSizeWords) *h_bad = *bad;
     __threadfence_system();

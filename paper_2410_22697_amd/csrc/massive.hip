@@ -47,14 +47,14 @@ inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
 // massive_sample_noalloc takes a step's per-step buffers (sizes, the two
 // gather lists, the write-through slots, the big-row list, the scan flags)
 // from this file-scope array instead of the context's. Layout: StepSizes
-// (256 B) | hbm list int2[kNoAllocMaxRows] | miss list int2[..] | write-through
+// (512 B) | hbm list int2[kNoAllocMaxRows] | miss list int2[..] | write-through
 // slots int32[..] | big rows int32[..] | scan flags uint64[kNoAllocFlagWords].
 // Each GPU holds its own copy (~30 MiB) while the library is loaded; its device
 // address is looked up once per device, in massive_init.
 constexpr int64_t kNoAllocMaxRows = 1310720;  // frontier rows (covers a 1,081,344-row bound)
 constexpr int64_t kNoAllocFlagWords = (int64_t(1) << 31) / 32 / ms::kScanTile + 2;  // any L + H < 2^31
-constexpr int64_t kNoAllocBytes = 256 + kNoAllocMaxRows * (8 + 8 + 4 + 4) + kNoAllocFlagWords * 8;
-static_assert(sizeof(ms::StepSizes) <= 256, "sizes fit the first 256 bytes");
+constexpr int64_t kNoAllocBytes = 512 + kNoAllocMaxRows * (8 + 8 + 4 + 4) + kNoAllocFlagWords * 8;
+static_assert(sizeof(ms::StepSizes) <= 512, "sizes fit the first 512 bytes");
 static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
 
 namespace {
@@ -821,7 +821,7 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
       }
       if (timed) c->pending.push_back({hop_a, hop_b, 6});
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));
-      ms::k_bits_scan<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, sz, k, sb.flags,
+      ms::k_bits_scan<<<(unsigned)nbw, ms::kScanNT, 0, s>>>(c->d_bits, c->W, c->L, sz, k, sb.flags,
                                                              epoch(), io->nodes, c->d_pos_of);
       if (k == c->K)
         ms::k_relabel<<<grid_for(eb[k - 1], ms::kScanTile, 1024), ms::kScanNT, 0, s>>>(io->indices[k - 1], sz, k,
@@ -899,7 +899,7 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   {
     const bool publish = pend >= 0 && c->H > 0;
     ms::k_step_done<<<publish ? grid_for(nb[c->K], 256, 1024) : 1, 256, 0, sm>>>(
-        sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, &c->d_ctr->bad,
+        sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, c->K, &c->d_ctr->bad,
         c->hd_sz + slot, c->hd_bad + slot);
   }
   CK(hipEventRecord(c->ev_batch_done[slot], sm));
@@ -1017,7 +1017,7 @@ int massive_sample_noalloc(massive_ctx* c, const int32_t* seeds, int32_t n0, mas
   uint8_t* base = c->d_scratch;
   StepBufs sb;
   sb.sz = reinterpret_cast<ms::StepSizes*>(base);
-  sb.hbm_list = reinterpret_cast<int2*>(base + 256);
+  sb.hbm_list = reinterpret_cast<int2*>(base + 512);
   sb.miss_list = sb.hbm_list + kNoAllocMaxRows;
   sb.miss_slot = reinterpret_cast<int32_t*>(sb.miss_list + kNoAllocMaxRows);
   sb.big = sb.miss_slot + kNoAllocMaxRows;

@@ -659,9 +659,11 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_blocks(SampleA
 // New nodes in ascending id: F[n_{k-1} + rank] = u, pos_of[u] = that
 // position, with the rank from the single-pass scan of the bitmap's
 // popcounts; the bitmap is cleared for the next hop. The last tile writes
-// n_k. (bits holds W + 4 words, the last four always zero.)
-__global__ __launch_bounds__(kScanNT) void k_bits_scan(uint32_t* __restrict__ bits, int64_t W, StepSizes* sz,
-                                                       int hop, uint64_t* flags, uint32_t epoch,
+// n_k. The new nodes below L (local ids) are the prefix at id L: the thread
+// whose words hold id L writes that count (the last tile, if every id is
+// below L). (bits holds W + 4 words, the last four always zero.)
+__global__ __launch_bounds__(kScanNT) void k_bits_scan(uint32_t* __restrict__ bits, int64_t W, int32_t L,
+                                                       StepSizes* sz, int hop, uint64_t* flags, uint32_t epoch,
                                                        int32_t* __restrict__ nodes, int32_t* __restrict__ pos_of) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   __shared__ uint32_t excl_lds;
@@ -675,6 +677,16 @@ __global__ __launch_bounds__(kScanNT) void k_bits_scan(uint32_t* __restrict__ bi
   const int32_t ex = block_exclusive_scan<kScanNT>(s, lds, &tot);
   const uint32_t before = lookback_exclusive(flags, blockIdx.x, (uint32_t)tot, epoch, &sz->status, &excl_lds);
   const int64_t n_prev = sz->n[hop - 1];
+  const int64_t wL = (int64_t)(L >> 5);
+  if (wL < W && wL >= base && wL < base + kScanItems) {
+    int32_t below = 0;
+#pragma unroll
+    for (int it = 0; it < kScanItems; ++it) {
+      if (base + it < wL) below += __popc(w[it]);
+      else if (base + it == wL) below += __popc(w[it] & ((1u << (L & 31)) - 1u));
+    }
+    sz->n_local_new[hop - 1] = (int64_t)before + ex + below;
+  }
   int64_t off = n_prev + before + ex;
 #pragma unroll
   for (int it = 0; it < kScanItems; ++it) {
@@ -691,7 +703,10 @@ __global__ __launch_bounds__(kScanNT) void k_bits_scan(uint32_t* __restrict__ bi
     }
     bits[base + it] = 0u;
   }
-  if (threadIdx.x == 0 && blockIdx.x == gridDim.x - 1) sz->n[hop] = n_prev + before + tot;
+  if (threadIdx.x == 0 && blockIdx.x == gridDim.x - 1) {
+    sz->n[hop] = n_prev + before + tot;
+    if (wL >= W) sz->n_local_new[hop - 1] = (int64_t)before + tot;  // every id is below L
+  }
 }
 
 // Relabel the last hop's sampled ids to their frontier positions (earlier

@@ -16,7 +16,7 @@ import random
 
 import pytest
 
-NT, WAVE, ITEMS = 256, 64, 2
+NT, WAVE, ITEMS = 256, 64, 4
 TILE = NT * ITEMS
 
 
@@ -68,7 +68,7 @@ def compact(cls, rnd):
     return hbm[:counters[0]], host[:counters[1]], counters
 
 
-@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 511, 512, 513, 2047, 2048, 2049, 5000])
+@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 1023, 1024, 1025, 2047, 2048, 2049, 5000])
 def test_every_row_lands_once_in_its_list(n):
     rnd = random.Random(n)
     for mix in ((0.3, 0.3, 0.3), (1.0, 0.0, 0.0), (0.0, 0.0, 1.0), (0.2, 0.5, 0.2)):
@@ -81,3 +81,8 @@ def test_every_row_lands_once_in_its_list(n):
         assert sorted(hbm) == [i for i in range(n) if cls[i] in (0, 1)]
         assert sorted(host) == [i for i in range(n) if cls[i] >= 2]
         assert counters == [sum(c in (0, 1) for c in cls), sum(c >= 2 for c in cls)]
+        # the completion kernel's counts: local rows come from the dedup scans,
+        # pending hits from their own counter; hits and misses from the lists
+        local, pending = sum(c == 0 for c in cls), sum(c == 3 for c in cls)
+        hits, misses = counters[0] - local + pending, counters[1] - pending
+        assert hits == sum(c in (1, 3) for c in cls) and misses == sum(c == 2 for c in cls)
