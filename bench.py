@@ -109,7 +109,7 @@ def frontier_keys(indptr, nodes, fanout):
 
 
 def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False, copy_probe=False,
-                first_alone=True, sampler_steps=0):
+                first_alone=True, sampler_steps=0, score_layout="rank"):
     """One context from init over steps 0..end-1 with look-ahead (`depth`
     batches in flight: step t is enqueued, after step t-1's round, before step
     t - depth + 1 is waited for, so the sampling of the next steps overlaps the
@@ -130,10 +130,13 @@ def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False,
     end = max([1] + [b for _, _, b, _ in windows])
     total = end + sampler_steps
     t0 = time.time()
+    free0 = torch.cuda.mem_get_info()[0]
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
-                 w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
+                 w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed, score_layout=score_layout,
+                 n_global=w.n)
     torch.cuda.synchronize()
     init_s = time.time() - t0
+    ctx_bytes = free0 - torch.cuda.mem_get_info()[0]  # device memory the context holds
     log("%s: massive_init %.2fs: cap=%d alpha=%.6g" % (w.name, init_s, gm.cap, gm.alpha))
     bbs = [gm.alloc_batch(w.batch) for _ in range(depth)]
     seeds_dev = [torch.from_numpy(np.ascontiguousarray(sched.seeds(t), np.int32)).cuda() for t in range(total)]
@@ -220,7 +223,7 @@ def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False,
         ms, calls = gm.timing()["sample_last_hop"]
         sampler = dict(ms=ms, calls=calls, keys=list(keys), steps=(pos, pos + sampler_steps))
         gm.set_timing(False)
-    out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, depth=depth,
+    out = dict(gm_cap=gm.cap, H=g.H, alpha=gm.alpha, init_s=init_s, depth=depth, ctx_bytes=ctx_bytes,
                stats=np.array(stats, np.float64), sizes=sizes, windows=out_w,
                first_steps=first_steps, state0=state0, sampler=sampler)
     del bbs, seeds_dev
@@ -480,6 +483,11 @@ def main():
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
                          "--copy-probe: the gather's HBM bytes over the headline window")
     ap.add_argument("--config-run", default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--layouts", action="store_true",
+                    help="the two S_A layouts of Section IV-B (over the halo in rank order, over every global "
+                         "id) on the same eviction run, each in its own process: device memory, round time, "
+                         "throughput, and that both give the same results; one JSON line each")
+    ap.add_argument("--layout-run", choices=("rank", "gid"), default=None, help=argparse.SUPPRESS)
     ap.add_argument("--sweep", action="store_true",
                     help="the paper's parameter grid (f in 15/25/35/50 %%, gamma in 0.95/0.995/0.9995, delta in "
                          "16..1024) on the same inputs, plus no buffer and one static run per f; one JSON line each")
@@ -506,6 +514,9 @@ def main():
     if args.compare and args.compare_mode is None:
         compare([a for a in sys.argv[1:]])
         return
+    if args.layouts:
+        layouts([a for a in sys.argv[1:] if a != "--layouts"])
+        return
 
     import synth
 
@@ -517,6 +528,9 @@ def main():
     g, local, store, sched = build_inputs(w, args.threads)
     if args.compare:
         print(json.dumps(compare_one(w, args.compare_mode, g, local, store, sched, args)), flush=True)
+        return
+    if args.layout_run:
+        print(json.dumps(layout_one(w, args.layout_run, g, local, store, sched, args)), flush=True)
         return
     if args.sweep:
         sweep(w, g, local, store, sched, args)
@@ -664,6 +678,48 @@ def pmc_summary(args):
     print("window_steps: %d..%d" % (head[0], head[1] - 1))
     print("traffic_bytes_per_launch: %d" % round(fe.mean() + wr.mean()))
     print("gather_source_sha256: %s" % hashlib.sha256(src[a:b].encode()).hexdigest())
+
+
+def layout_one(w, layout, g, local, store, sched, args):
+    """One S_A layout on the eviction run from init (five rounds), every
+    kernel group timed: device memory of the context, the score arrays' bytes,
+    the round's time, throughput, and a digest of every step's counts and the
+    final state for the cross-check."""
+    import hashlib
+    n = EVICTION_RUN_ROUNDS * w.delta + 1
+    res = run_context(w, g, local, store, sched, [("run", 0, n, True)], args.depth, first_alone=False,
+                      score_layout=layout)
+    sm = summarize(w, res, "run")
+    tim = res["windows"]["run"]["tim"]
+    # local, hits, misses, rows per step (the host-link rows depend on when a refill lands)
+    digest = hashlib.sha256(np.ascontiguousarray(res["stats"][:n, :4]).tobytes()).hexdigest()[:16]
+    score_bytes = 4 * g.H if layout == "rank" else 8 * w.n
+    return {"metric": "eviction run with the S_A layout %r" % layout, "layout": layout, "workload": w.name,
+            "steps": n, "value": sm["value"], "unit": "minibatches/s", "eviction_rounds": sm["eviction_rounds"],
+            "evicted_rows": sm["evicted_rows"], "hit_rate": sm["hit_rate"],
+            "round_ms": round(tim["evict_round"][0] / max(tim["evict_round"][1], 1), 3),
+            "score_array_bytes": score_bytes, "context_device_bytes": int(res["ctx_bytes"]),
+            "init_s": round(res["init_s"], 3), "counts_digest": digest}
+
+
+def layouts(argv):
+    """Both S_A layouts on the same run, each in a process of its own."""
+    import subprocess
+    outs = []
+    for layout in ("rank", "gid"):
+        cmd = [sys.executable, os.path.abspath(__file__)] + argv + ["--layout-run", layout]
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            raise SystemExit("bench: the layout run %s failed with status %d" % (layout, r.returncode))
+        outs.append(json.loads([l for l in r.stdout.splitlines() if l.startswith("{")][-1]))
+    same = outs[0]["counts_digest"] == outs[1]["counts_digest"] and outs[0]["evicted_rows"] == outs[1]["evicted_rows"]
+    for o in outs:
+        o["same_results_as_other_layout"] = same
+        log("layout %-4s: %.1f minibatches/s, round %.3f ms, scores %.1f MB, context %.2f GB" %
+            (o["layout"], o["value"], o["round_ms"], o["score_array_bytes"] / 1e6, o["context_device_bytes"] / 1e9))
+        print(json.dumps(o), flush=True)
+    if not same:
+        raise SystemExit("bench: the two layouts gave different results")
 
 
 COMPARE_MODES = ("no_buffer", "static", "eviction")

@@ -60,6 +60,11 @@ extern "C" {
 #define MASSIVE_ESTATE (-5)    /* call out of order (see massive_sample)      */
 
 #define MASSIVE_MAX_HOPS 8
+
+/* S_A layouts (massive_init_args.score_layout), the two the paper weighs in
+ * Section IV-B: an array over the halo only, or one over every global id */
+#define MASSIVE_SCORES_BY_RANK 0 /* S_A over the H halo nodes, in rank order */
+#define MASSIVE_SCORES_BY_GID 1  /* S_A over all n_global global ids, indexed by id */
 #define MASSIVE_MAX_INFLIGHT 3 /* batches enqueued and not yet waited for */
 
 typedef struct massive_ctx massive_ctx;
@@ -85,12 +90,22 @@ typedef struct {
   int32_t delta;              /* eviction interval, >= 1                      */
   uint64_t seed;              /* Philox key                                   */
   void* stream;               /* hipStream_t for all work (NULL: default)     */
+  int32_t score_layout;       /* MASSIVE_SCORES_BY_RANK (0, the default) or
+                                 MASSIVE_SCORES_BY_GID: S_A (and a rank per
+                                 id) over every global id, 8 B per id; the
+                                 eviction round then selects over all ids  */
+  int64_t n_global;           /* MASSIVE_SCORES_BY_GID: the global id space,
+                                 every halo_gid in [0, n_global) and distinct,
+                                 n_global <= 2^31; ignored otherwise         */
 } massive_init_args;
 
 /* Creates a context: uploads G_p and local features to HBM, ranks the halo,
  * fills the HBM buffer with the cap best-ranked halo rows from halo_store,
- * and sets S_E = 1, S_A = -1 / 0. On failure *out is NULL and the message is
- * in massive_last_error(NULL). */
+ * and sets S_E = 1, S_A = -1 / 0. Both score layouts give the same results
+ * (states, eviction and replacement sets); they differ in memory and in the
+ * eviction round's time. MASSIVE_EINVAL for a halo_gid outside [0, n_global)
+ * or repeated (BY_GID). On failure *out is NULL and the message is in
+ * massive_last_error(NULL). */
 int massive_init(const massive_init_args* args, massive_ctx** out);
 
 /* Upper bounds on the output sizes of a batch of n_seeds seeds:

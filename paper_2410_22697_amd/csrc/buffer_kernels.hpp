@@ -80,8 +80,8 @@ struct ClassifyArgs {
   const uint64_t* tab;
   uint32_t tmask;
   int32_t* hitcnt;
-  float* S_A;                 // by halo rank
-  const int32_t* rank_of;     // halo id -> rank
+  float* S_A;                 // by halo rank, or by global id
+  const int32_t* sa_idx;      // halo id -> its S_A index (rank, or global id)
   int32_t* pos_of;
   uint8_t* mask;
   int2* hbm_list;
@@ -107,7 +107,7 @@ constexpr int kClsBlocks = 512;  // grid bound: the blocks stride over the front
 // frontier ids; a window of four table entries from each id's probe start
 // (the 16-byte pairs holding entries p & ~1 .. (p & ~1) + 3, which settle
 // almost every search; the rare rest probes on one by one); the misses'
-// ranks (S_A is kept by rank) and, while a refill is in flight, the hit
+// S_A indices (rank or global id) and, while a refill is in flight, the hit
 // slots' refill stamps. Lanes past the end and local rows load dummy
 // (in-range) addresses and change nothing.
 __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
 #pragma unroll
     for (int it = 0; it < kClsItems; ++it) {
       const int32_t sl = slot[it] >= 0 ? slot[it] : 0;
-      rk[it] = a.rank_of[v[it] >= a.L && slot[it] < 0 ? v[it] - a.L : 0];
+      rk[it] = a.sa_idx[v[it] >= a.L && slot[it] < 0 ? v[it] - a.L : 0];
       sr[it] = 0;
       ld[it] = 0;
       if (pending) {  // the same in every lane
@@ -532,6 +532,8 @@ __global__ void k_round_setup(RoundState* __restrict__ rs, Counters* __restrict_
   rs->need = k;
   rs->prefix = 0;
   rs->pmask = 0;
+  rs->prefix_lo = 0;
+  rs->pmask_lo = 0;
   rs->nE_sel = k < rs->nE ? rs->nE : 0;
   rs->k_sel = k < rs->nE ? k : 0;
   if (k > 0) {
@@ -601,7 +603,7 @@ __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ S
 }
 
 __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs, uint32_t* __restrict__ ghist,
-                                                     int shift, int32_t* __restrict__ bad) {
+                                                     int shift, int32_t* __restrict__ bad, int lo_word = 0) {
   __shared__ int64_t lds[256 / MS_WAVE + 1];
   __shared__ int32_t pick;
   __shared__ int64_t before;
@@ -627,8 +629,13 @@ __global__ __launch_bounds__(256) void k_select_pick(RoundState* __restrict__ rs
       rs->need = 0;
     } else {
       rs->need = need - before;
-      rs->prefix |= (uint32_t)pick << shift;
-      rs->pmask |= 255u << shift;
+      if (lo_word) {
+        rs->prefix_lo |= (uint32_t)pick << shift;
+        rs->pmask_lo |= 255u << shift;
+      } else {
+        rs->prefix |= (uint32_t)pick << shift;
+        rs->pmask |= 255u << shift;
+      }
     }
   }
 }
@@ -717,11 +724,154 @@ __global__ __launch_bounds__(kScanNT) void k_rank_emit(const float* __restrict__
   }
 }
 
-// S_A by halo id from S_A by rank (for export).
-__global__ void k_scores_by_id(const float* __restrict__ S_A, const int32_t* __restrict__ h_of_rank, int64_t H,
+// S_A by halo id (for export), from either layout.
+__global__ void k_scores_by_id(const float* __restrict__ S_A, const int32_t* __restrict__ sa_idx, int64_t H,
                                float* __restrict__ out) {
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < H; r += (int64_t)gridDim.x * blockDim.x)
-    out[h_of_rank[r]] = S_A[r];
+  for (int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; h < H; h += (int64_t)gridDim.x * blockDim.x)
+    out[h] = S_A[sa_idx[h]];
+}
+
+// ---------------------------------------- replacement select, S_A by global id
+// With S_A over every global id g (non-halo ids hold -1 and are never
+// candidates), the scan runs in id order, not rank order, so the rank is part
+// of the key: candidate g has the 64-bit key (cand_key(S_A[g]), rank_g[g]),
+// unique per candidate. An exact radix select over it, 8 bits per pass from
+// the top (four passes on the score word, then four on the rank word), finds
+// the k'-th smallest key T; the replacements are exactly the keys <= T, which
+// are emitted and sorted by (score, rank). Each thread takes four
+// consecutive entries per iteration; a wave adds the lanes whose digit equals
+// its first active lane's with one LDS atomic.
+__global__ __launch_bounds__(256) void k_gselect_hist(const float* __restrict__ S, const int32_t* __restrict__ rank_g,
+                                                      int64_t n, const RoundState* __restrict__ rs, int lo_word,
+                                                      int shift, uint32_t* __restrict__ ghist) {
+  __shared__ uint32_t hist[256];
+  if (rs->k == 0) return;
+  hist[threadIdx.x] = 0;
+  __syncthreads();
+  const uint32_t ph = rs->prefix, mh = rs->pmask, pl = rs->prefix_lo, ml = rs->pmask_lo;
+  const int lane = lane_id();
+  const int64_t n4 = n / 4;
+  const float4* S4 = reinterpret_cast<const float4*>(S);
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < (n + 3) / 4;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    float a[4] = {-1.0f, -1.0f, -1.0f, -1.0f};
+    if (q < n4) {
+      const float4 x = S4[q];
+      a[0] = x.x;
+      a[1] = x.y;
+      a[2] = x.z;
+      a[3] = x.w;
+    } else {
+      for (int j = 0; j < 4; ++j)
+        if (4 * q + j < n) a[j] = S[4 * q + j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t k = cand_key(a[j]);
+      bool in = a[j] >= 0.0f && (k & mh) == ph;
+      uint32_t r = 0;
+      if (lo_word && in) r = (uint32_t)rank_g[4 * q + j];
+      in = in && (!lo_word || (r & ml) == pl);
+      const uint32_t d = ((lo_word ? r : k) >> shift) & 255u;
+      const uint64_t m = ballot(in);
+      if (!m) continue;
+      const int first = __ffsll((unsigned long long)m) - 1;
+      const uint32_t d0 = __shfl(d, first, MS_WAVE);
+      const uint64_t same = ballot(in && d == d0);
+      if (lane == first) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+      else if (in && d != d0) atomicAdd(&hist[d], 1u);
+    }
+  }
+  __syncthreads();
+  if (hist[threadIdx.x]) atomicAdd(&ghist[threadIdx.x], hist[threadIdx.x]);
+}
+
+__device__ __forceinline__ bool gsel_in(float a, uint32_t r, uint32_t th, uint32_t tl) {
+  if (!(a >= 0.0f)) return false;
+  const uint32_t k = cand_key(a);
+  return k < th || (k == th && r <= tl);
+}
+
+// Per tile of kScanTile ids: how many replacements (keys <= T) it holds.
+__global__ __launch_bounds__(kScanNT) void k_gsel_count(const float* __restrict__ S, const int32_t* __restrict__ rank_g,
+                                                        int64_t n, const RoundState* __restrict__ rs,
+                                                        int32_t* __restrict__ partials) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  const bool on = rs->k > 0;
+  const uint32_t th = rs->prefix, tl = rs->prefix_lo;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  int32_t c = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t g = base + (int64_t)it * kScanNT + threadIdx.x;
+    if (on && g < n) {
+      const float a = S[g];
+      if (a >= 0.0f) c += gsel_in(a, (uint32_t)rank_g[g], th, tl);
+    }
+  }
+  c = block_sum<kScanNT>(c, lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = c;
+}
+
+// Emits the replacements in id order as (rank, halo id) pairs at the tile's
+// prefix (partials scanned by k_scan_partials).
+__global__ __launch_bounds__(kScanNT) void k_gsel_emit(const float* __restrict__ S, const int32_t* __restrict__ rank_g,
+                                                       const int32_t* __restrict__ h_of_rank, int64_t n,
+                                                       const RoundState* __restrict__ rs,
+                                                       const int32_t* __restrict__ partials, uint32_t* __restrict__ keys,
+                                                       int32_t* __restrict__ vals) {
+  __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
+  if (rs->k == 0) return;
+  const uint32_t th = rs->prefix, tl = rs->prefix_lo;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  bool f[kScanItems];
+  int32_t r[kScanItems];
+  int32_t c = 0;
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it) {
+    const int64_t g = base + it;
+    const float a = g < n ? S[g] : -1.0f;
+    r[it] = a >= 0.0f ? rank_g[g] : 0;
+    f[it] = gsel_in(a, (uint32_t)r[it], th, tl);
+    c += f[it];
+  }
+  int32_t tot;
+  int64_t o = (int64_t)block_exclusive_scan<kScanNT>(c, lds, &tot) + partials[blockIdx.x];
+#pragma unroll
+  for (int it = 0; it < kScanItems; ++it)
+    if (f[it]) {
+      keys[o] = (uint32_t)r[it];
+      vals[o] = h_of_rank[r[it]];
+      ++o;
+    }
+}
+
+// After the sort by rank: each pair's key becomes its candidate key (the
+// score word), for the stable sort that puts them in (score, rank) order.
+__global__ void k_gsel_keys(const int32_t* __restrict__ vals, const int64_t* __restrict__ n_ptr,
+                            const float* __restrict__ S, const int32_t* __restrict__ sa_idx,
+                            uint32_t* __restrict__ keys) {
+  const int64_t n = *n_ptr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    keys[i] = cand_key(S[sa_idx[vals[i]]]);
+}
+
+// Scores by global id, at init: S_A[gid[h]] = 0 and rank_g[gid[h]] = rank of h
+// for every halo node (the rest of both arrays was filled with -1).
+__global__ void k_gid_init(const int32_t* __restrict__ gid, const int32_t* __restrict__ rank_of, int64_t H,
+                           float* __restrict__ S, int32_t* __restrict__ rank_g) {
+  for (int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; h < H; h += (int64_t)gridDim.x * blockDim.x) {
+    S[gid[h]] = 0.0f;
+    rank_g[gid[h]] = rank_of[h];
+  }
+}
+
+// Repeated global ids would share an S_A entry: after k_gid_init, an id whose
+// rank entry is not its own halo node's rank was written twice.
+__global__ void k_gid_check(const int32_t* __restrict__ gid, const int32_t* __restrict__ rank_of, int64_t H,
+                            const int32_t* __restrict__ rank_g, int32_t* __restrict__ bad) {
+  for (int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; h < H; h += (int64_t)gridDim.x * blockDim.x)
+    if (rank_g[gid[h]] != rank_of[h]) atomicOr(bad, 4);
 }
 
 // ------------------------------------------------------ stable radix sort
@@ -862,16 +1012,16 @@ __global__ void k_rank_finish(const int32_t* __restrict__ h_of_rank, int64_t H, 
     rank_of[h_of_rank[r]] = (int32_t)r;
 }
 
-// Initial buffer: slot s holds the halo node of rank s (S_A is by rank).
+// Initial buffer: slot s holds the halo node of rank s.
 __global__ void k_init_buffer(const int32_t* __restrict__ h_of_rank, int64_t cap, int32_t L,
                               int32_t* __restrict__ slot_id, float* __restrict__ S_E, int32_t* __restrict__ hitcnt,
-                              float* __restrict__ S_A, int2* __restrict__ fill) {
+                              float* __restrict__ S_A, const int32_t* __restrict__ sa_idx, int2* __restrict__ fill) {
   for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < cap; s += (int64_t)gridDim.x * blockDim.x) {
     const int32_t h = h_of_rank[s];
     slot_id[s] = h;
     S_E[s] = 1.0f;
     hitcnt[s] = 0;
-    S_A[s] = -1.0f;
+    S_A[sa_idx[h]] = -1.0f;
     fill[s] = make_int2((int32_t)(L + s), h);
   }
 }
@@ -903,10 +1053,11 @@ __global__ void k_esel_keys_slot(const int32_t* __restrict__ vals, const int64_t
 // ------------------------------------------------------------------ swap
 // Pair E[i] (ascending slot) with R[i]; every read sees pre-round values
 // because the slots, the evicted nodes and the replacements are all
-// distinct, so no two threads touch the same entry. S_A is by rank.
+// distinct, so no two threads touch the same entry. S_A is reached through
+// each node's S_A index (its rank, or its global id).
 __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict__ R, const int64_t* __restrict__ k_ptr,
                        int32_t L, int64_t cap, int32_t H, int32_t* __restrict__ slot_id, float* __restrict__ S_E,
-                       float* __restrict__ S_A, const int32_t* __restrict__ rank_of,
+                       float* __restrict__ S_A, const int32_t* __restrict__ sa_idx,
                        int32_t* __restrict__ out_ev, int32_t* __restrict__ out_slot,
                        int32_t* __restrict__ out_rep, int2* __restrict__ fill, int32_t* __restrict__ bad,
                        int32_t* __restrict__ slot_round, int32_t round_id) {
@@ -919,7 +1070,7 @@ __global__ void k_swap(const int32_t* __restrict__ E, const int32_t* __restrict_
       continue;
     }
     const int32_t e = slot_id[s];
-    const int32_t re = rank_of[e], rr = rank_of[r];
+    const int32_t re = sa_idx[e], rr = sa_idx[r];
     const float se = S_E[s], sa = S_A[rr];
     S_A[re] = se;
     S_E[s] = sa;

@@ -134,7 +134,8 @@ struct RoundState {
   int64_t nE, nC;          // |E|, |C|
   int64_t k;               // k' = min(|E|, |C|)
   int64_t need;            // ties at the threshold still to take
-  uint32_t prefix, pmask;  // radix-select prefix of the threshold key
+  uint32_t prefix, pmask;  // radix-select prefix of the threshold key (S_A word)
+  uint32_t prefix_lo, pmask_lo;  // ... and of its rank word (scores by global id)
   int64_t n_lt, n_eq;      // candidates strictly before / equal to the threshold
   int64_t nE_sel, k_sel;   // |E| and k' when k' < |E| (E must be narrowed), else 0
 };

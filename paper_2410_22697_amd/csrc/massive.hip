@@ -131,6 +131,16 @@ struct massive_ctx {
   float* d_S_A = nullptr;
   int32_t* d_rank_of = nullptr;
   int32_t* d_h_of_rank = nullptr;
+  // S_A layout: by rank (H entries; a node's S_A index is its rank) or by
+  // global id (n_global entries; its index is its global id, and rank_g gives
+  // the rank of the halo node with each id)
+  int32_t layout = MASSIVE_SCORES_BY_RANK;
+  int64_t n_sa = 0;                  // entries of S_A
+  const int32_t* d_sa_idx = nullptr; // [H] S_A index of halo h (d_rank_of or d_gid)
+  int32_t* d_gid = nullptr;          // [H] global id of halo h
+  int32_t* d_rank_g = nullptr;       // [n_global] by global id: rank of that halo node, -1 elsewhere
+  int32_t* d_gpart = nullptr;        // tile partials of the global-id selection
+  int64_t* d_deg = nullptr;          // [H] degrees, during init only
   uint64_t* d_tab = nullptr;
   int32_t* d_pos_of = nullptr;
   uint32_t* d_bits = nullptr;
@@ -419,7 +429,8 @@ void free_ctx(massive_ctx* c) {
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
                  c->d_part, c->d_part2, c->d_scan_flags, c->d_dummy, c->d_E, c->d_R,
                  c->d_fill, c->d_ctr, c->d_slot_round, c->d_landed,
-                 c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big};
+                 c->d_k0, c->d_k1, c->d_v0, c->d_v1, c->d_hist, c->d_ghist, c->d_big,
+                 c->d_gid, c->d_rank_g, c->d_gpart, c->d_deg};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   for (int i = 0; i < kSlots; ++i)
@@ -457,6 +468,8 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   c->seed = a->seed;
   c->nnz = a->indptr[c->R];
   c->cap = (int64_t)a->H * a->buffer_pct / 100;
+  c->layout = a->score_layout;
+  c->n_sa = c->layout == MASSIVE_SCORES_BY_GID ? a->n_global : a->H;
   c->hcap = 64;
   while (c->hcap < 2 * c->cap) c->hcap <<= 1;
   c->hmask = (uint32_t)(c->hcap - 1);
@@ -524,9 +537,18 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CKA(c->d_slot_id, cap * 4);
   CKA(c->d_S_E, cap * 4);
   CKA(c->d_hitcnt, cap * 4);
-  CKA(c->d_S_A, H * 4);
+  CKA(c->d_S_A, c->n_sa * 4);
+  CKA(c->d_gid, H * 4);
+  if (c->layout == MASSIVE_SCORES_BY_GID) {
+    CKA(c->d_rank_g, c->n_sa * 4);
+    CKA(c->d_gpart, (cdiv(c->n_sa, ms::kScanTile) + 8) * 4);
+  }
   CKA(c->d_rank_of, H * 4);
   CKA(c->d_h_of_rank, H * 4);
+  // a node's S_A index: its global id or its rank (classify reads entry 0 of
+  // this array for rows that are not misses, so it is set whatever H is)
+  c->d_sa_idx = c->layout == MASSIVE_SCORES_BY_GID ? c->d_gid : c->d_rank_of;
+  if (!c->d_sa_idx) return c->fail(MASSIVE_EHIP, "no S_A index array");
   CKA(c->d_tab, c->hcap * 8);
   CKA(c->d_pos_of, R * 4);
   CKA(c->d_big, R * 4);
@@ -588,26 +610,36 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
 
   if (H > 0) {
     // halo rank: (degree desc, global id asc) by two stable radix sorts
-    int32_t* d_gid = nullptr;
-    int64_t* d_deg = nullptr;
-    CKA(d_gid, H * 4);
-    CKA(d_deg, H * 8);
-    CK(hipMemcpyAsync(d_gid, a->halo_gid, H * 4, hipMemcpyHostToDevice, s));
-    CK(hipMemcpyAsync(d_deg, a->halo_degree, H * 8, hipMemcpyHostToDevice, s));
-    ms::k_rank_keys_lo<<<grid_for(H, 256), 256, 0, s>>>(d_gid, H, c->d_k0, c->d_v0);
+    CKA(c->d_deg, H * 8);
+    CK(hipMemcpyAsync(c->d_gid, a->halo_gid, H * 4, hipMemcpyHostToDevice, s));
+    CK(hipMemcpyAsync(c->d_deg, a->halo_degree, H * 8, hipMemcpyHostToDevice, s));
+    ms::k_rank_keys_lo<<<grid_for(H, 256), 256, 0, s>>>(c->d_gid, H, c->d_k0, c->d_v0);
     sort_u32(c, s, nullptr, H, H, nullptr);
-    ms::k_rank_keys_hi<<<grid_for(H, 256), 256, 0, s>>>(d_deg, c->d_v0, H, c->d_k0);
+    ms::k_rank_keys_hi<<<grid_for(H, 256), 256, 0, s>>>(c->d_deg, c->d_v0, H, c->d_k0);
     sort_u32(c, s, nullptr, H, H, c->d_h_of_rank);
     ms::k_rank_finish<<<grid_for(H, 256), 256, 0, s>>>(c->d_h_of_rank, H, c->d_rank_of);
-    ms::k_fill<float><<<grid_for(H, 256), 256, 0, s>>>(c->d_S_A, H, 0.0f);
+    if (c->layout == MASSIVE_SCORES_BY_GID) {
+      // S_A and the rank of every global id: -1 except at halo ids
+      ms::k_fill<float><<<grid_for(c->n_sa, 256), 256, 0, s>>>(c->d_S_A, c->n_sa, -1.0f);
+      ms::k_fill<int32_t><<<grid_for(c->n_sa, 256), 256, 0, s>>>(c->d_rank_g, c->n_sa, -1);
+      ms::k_gid_init<<<grid_for(H, 256), 256, 0, s>>>(c->d_gid, c->d_rank_of, H, c->d_S_A, c->d_rank_g);
+      CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
+      ms::k_gid_check<<<grid_for(H, 256), 256, 0, s>>>(c->d_gid, c->d_rank_of, H, c->d_rank_g, &c->d_ctr->bad);
+      CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
+      CK(hipStreamSynchronize(s));
+      if (c->h_ctr->bad) return c->fail(MASSIVE_EINVAL, "halo_gid repeats a global id");
+      CK(hipMemsetAsync(c->d_ctr, 0, sizeof(ms::Counters), s));
+    } else {
+      ms::k_fill<float><<<grid_for(H, 256), 256, 0, s>>>(c->d_S_A, H, 0.0f);
+    }
     CK(hipStreamSynchronize(s));
-    (void)hipFree(d_gid);
-    (void)hipFree(d_deg);
+    (void)hipFree(c->d_deg);
+    c->d_deg = nullptr;
   }
   ms::k_fill<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty);
   if (cap > 0) {
     ms::k_init_buffer<<<grid_for(cap, 256), 256, 0, s>>>(c->d_h_of_rank, cap, c->L, c->d_slot_id, c->d_S_E,
-                                                         c->d_hitcnt, c->d_S_A, c->d_fill);
+                                                         c->d_hitcnt, c->d_S_A, c->d_sa_idx, c->d_fill);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, nullptr);
     // the cap best-ranked rows arrive over the host link
     c->h_rs->k = cap;
@@ -658,6 +690,13 @@ int massive_init(const massive_init_args* a, massive_ctx** out) {
   if (a->buffer_pct < 0 || a->buffer_pct > 100) return bad("buffer_pct must be in 0..100");
   if (!(a->gamma > 0.0f && a->gamma <= 1.0f)) return bad("gamma must be in (0, 1]");
   if (a->delta < 1) return bad("delta must be >= 1");
+  if (a->score_layout != MASSIVE_SCORES_BY_RANK && a->score_layout != MASSIVE_SCORES_BY_GID)
+    return bad("score_layout must be MASSIVE_SCORES_BY_RANK or MASSIVE_SCORES_BY_GID");
+  if (a->score_layout == MASSIVE_SCORES_BY_GID) {
+    if (a->n_global < 1 || a->n_global > (int64_t(1) << 31)) return bad("n_global must be in 1..2^31");
+    for (int32_t h = 0; h < a->H; ++h)
+      if (a->halo_gid[h] < 0 || a->halo_gid[h] >= a->n_global) return bad("a halo_gid lies outside [0, n_global)");
+  }
   const int64_t R = (int64_t)a->L + a->H;
   if (a->indptr[0] != 0 || a->indptr[R] < 0) return bad("indptr must start at 0");
   massive_ctx* c = new (std::nothrow) massive_ctx();
@@ -858,7 +897,7 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
     ca.tmask = c->hmask;
     ca.hitcnt = c->d_hitcnt;
     ca.S_A = c->d_S_A;
-    ca.rank_of = c->d_rank_of;
+    ca.sa_idx = c->d_sa_idx;
     ca.pos_of = c->d_pos_of;
     ca.mask = io->mask;
     ca.hbm_list = sb.hbm_list;
@@ -1083,20 +1122,41 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
       sort_u32(c, s, &rs->k_sel, 0, cap, c->d_E);
     }
     ms::k_fill_gated<int32_t><<<grid_for(cap, 256), 256, 0, s>>>(c->d_R, cap, -1, &rs->k);
-    // radix select of the k'-th candidate key, 8 bits per pass
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      ms::k_select_hist<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, rs, shift, c->d_ghist);
-      ms::k_select_pick<<<1, 256, 0, s>>>(rs, c->d_ghist, shift, &c->d_ctr->bad);
+    if (c->layout == MASSIVE_SCORES_BY_GID) {
+      // S_A over every global id, scanned in id order: an exact radix select
+      // over the 64-bit key (score word, rank), then the k' keys below or at
+      // it, sorted by rank and then stably by score
+      const int64_t n = c->n_sa;
+      for (int word = 0; word < 2; ++word)
+        for (int shift = 24; shift >= 0; shift -= 8) {
+          ms::k_gselect_hist<<<grid_for(cdiv(n, 4), 256, 4096), 256, 0, s>>>(c->d_S_A, c->d_rank_g, n, rs, word,
+                                                                           shift, c->d_ghist);
+          ms::k_select_pick<<<1, 256, 0, s>>>(rs, c->d_ghist, shift, &c->d_ctr->bad, word);
+        }
+      const int64_t nbg = std::max<int64_t>(1, cdiv(n, ms::kScanTile));
+      ms::k_gsel_count<<<(unsigned)nbg, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_rank_g, n, rs, c->d_gpart);
+      ms::k_scan_partials<<<1, ms::kScanNT, 0, s>>>(c->d_gpart, nbg, nullptr, nullptr);
+      ms::k_gsel_emit<<<(unsigned)nbg, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_rank_g, c->d_h_of_rank, n, rs,
+                                                            c->d_gpart, c->d_k0, c->d_v0);
+      sort_u32(c, s, &rs->k, 0, cap, nullptr);
+      ms::k_gsel_keys<<<grid_for(cap, 256), 256, 0, s>>>(c->d_v0, &rs->k, c->d_S_A, c->d_sa_idx, c->d_k0);
+      sort_u32(c, s, &rs->k, 0, cap, c->d_R);
+    } else {
+      // radix select of the k'-th candidate key, 8 bits per pass
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        ms::k_select_hist<<<grid_for(H, 256, 2048), 256, 0, s>>>(c->d_S_A, H, rs, shift, c->d_ghist);
+        ms::k_select_pick<<<1, 256, 0, s>>>(rs, c->d_ghist, shift, &c->d_ctr->bad);
+      }
+      const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
+      ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, H, rs, c->d_part, c->d_part2);
+      ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2,
+                                                            c->d_k0, c->d_v0, c->d_R);
+      // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
+      sort_u32(c, s, &rs->n_lt, 0, cap, c->d_R);
     }
-    const int64_t nbh = std::max<int64_t>(1, cdiv(H, ms::kScanTile));
-    ms::k_rank_count<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, H, rs, c->d_part, c->d_part2);
-    ms::k_rank_emit<<<(unsigned)nbh, ms::kScanNT, 0, s>>>(c->d_S_A, c->d_h_of_rank, H, rs, c->d_part, c->d_part2,
-                                                          c->d_k0, c->d_v0, c->d_R);
-    // candidates before the threshold: stable sort by key (S_A desc), rank order kept for ties
-    sort_u32(c, s, &rs->n_lt, 0, cap, c->d_R);
     c->round_id += 1;
     ms::k_swap<<<grid_for(cap, 256), 256, 0, s>>>(c->d_E, c->d_R, &rs->k, c->L, cap, c->H, c->d_slot_id, c->d_S_E,
-                                                  c->d_S_A, c->d_rank_of, evicted, slots, replaced, c->d_fill, &c->d_ctr->bad,
+                                                  c->d_S_A, c->d_sa_idx, evicted, slots, replaced, c->d_fill, &c->d_ctr->bad,
                                                   c->d_slot_round, c->round_id);
     ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
@@ -1149,10 +1209,10 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
   if (slot_id && c->cap) CK(hipMemcpyAsync(slot_id, c->d_slot_id, c->cap * 4, hipMemcpyDeviceToHost, s));
   if (S_E && c->cap) CK(hipMemcpyAsync(S_E, c->d_S_E, c->cap * 4, hipMemcpyDeviceToHost, s));
   if (S_A && c->H) {
-    // S_A is kept by halo rank; export it by halo id (through a sort buffer,
-    // free once the last round has completed)
+    // S_A is kept by halo rank or by global id; export it by halo id (through
+    // a sort buffer, free once the last round has completed)
     float* by_id = reinterpret_cast<float*>(c->d_v1);
-    ms::k_scores_by_id<<<grid_for(c->H, 256), 256, 0, s>>>(c->d_S_A, c->d_h_of_rank, c->H, by_id);
+    ms::k_scores_by_id<<<grid_for(c->H, 256), 256, 0, s>>>(c->d_S_A, c->d_sa_idx, c->H, by_id);
     CK(hipMemcpyAsync(S_A, by_id, (int64_t)c->H * 4, hipMemcpyDeviceToHost, s));
   }
   CK(hipStreamSynchronize(s));

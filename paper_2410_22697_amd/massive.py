@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libmassive.so")
 MAX_HOPS = 8
 
 OK, EINVAL, ECAPACITY, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
+SCORES_BY_RANK, SCORES_BY_GID = 0, 1  # S_A layouts (Section IV-B)
 MAX_INFLIGHT = 3  # batches enqueued with sample_async and not yet waited for
 _NAMES = {EINVAL: "EINVAL", ECAPACITY: "ECAPACITY", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE"}
 
@@ -39,7 +40,7 @@ class InitArgs(ctypes.Structure):
                 ("row_bytes", ctypes.c_int64), ("K", ctypes.c_int32),
                 ("fanout", ctypes.c_int32 * MAX_HOPS), ("buffer_pct", ctypes.c_int32),
                 ("gamma", ctypes.c_float), ("delta", ctypes.c_int32), ("seed", ctypes.c_uint64),
-                ("stream", ctypes.c_void_p)]
+                ("stream", ctypes.c_void_p), ("score_layout", ctypes.c_int32), ("n_global", ctypes.c_int64)]
 
 
 class Batch(ctypes.Structure):
@@ -146,7 +147,9 @@ class Massive:
 
     def __init__(self, L, H, indptr, indices, halo_gid, halo_degree, local_feat, halo_store,
                  row_bytes, fanout: Sequence[int], buffer_pct: int, gamma: float, delta: int,
-                 seed: int = 0, stream=None):
+                 seed: int = 0, stream=None, score_layout: str = "rank", n_global: int = 0):
+        """score_layout: "rank" (S_A over the halo, in rank order) or "gid"
+        (S_A over all n_global global ids)."""
         import torch
         self._torch = torch
         self._lib = load()
@@ -185,6 +188,11 @@ class Massive:
             a.fanout[i] = int(f)
         a.buffer_pct, a.gamma, a.delta, a.seed = int(buffer_pct), float(gamma), int(delta), int(seed)
         a.stream = int(stream.cuda_stream)
+        if score_layout not in ("rank", "gid"):
+            raise ValueError("score_layout must be 'rank' or 'gid'")
+        a.score_layout = SCORES_BY_GID if score_layout == "gid" else SCORES_BY_RANK
+        a.n_global = int(n_global)
+        self.score_layout = score_layout
         h = ctypes.c_void_p()
         rc = self._lib.massive_init(ctypes.byref(a), ctypes.byref(h))
         if rc != OK:

@@ -32,14 +32,18 @@ def pinned_store(prob: Problem):
 
 
 def make_gpu(prob: Problem, store=None, **over):
+    """A context on prob; over may set fanout, buffer_pct, gamma, delta, seed,
+    and score_layout ("rank" or "gid", with n_global)."""
     from paper_2410_22697_amd import Massive
-    kw = dict(fanout=prob.fanout, buffer_pct=prob.buffer_pct, gamma=prob.gamma, delta=prob.delta, seed=prob.seed)
+    kw = dict(fanout=prob.fanout, buffer_pct=prob.buffer_pct, gamma=prob.gamma, delta=prob.delta, seed=prob.seed,
+              score_layout="rank", n_global=0)
     kw.update(over)
     if store is None:
         store = pinned_store(prob)
     lf = np.ascontiguousarray(prob.local_feat).view(np.uint8).reshape(prob.L, prob.row_bytes)
     return Massive(prob.L, prob.H, prob.indptr, prob.indices, prob.halo_gid, prob.halo_degree, lf, store,
-                   prob.row_bytes, kw["fanout"], kw["buffer_pct"], kw["gamma"], kw["delta"], kw["seed"])
+                   prob.row_bytes, kw["fanout"], kw["buffer_pct"], kw["gamma"], kw["delta"], kw["seed"],
+                   score_layout=kw["score_layout"], n_global=kw["n_global"])
 
 
 def to_dev(a):

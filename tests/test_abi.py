@@ -29,7 +29,7 @@ def test_binding_constants_match_the_header():
     assert int(defs["MASSIVE_MAX_HOPS"]) == massive.MAX_HOPS
     assert int(defs["MASSIVE_MAX_INFLIGHT"]) == massive.MAX_INFLIGHT
     assert int(defs["MASSIVE_TIMING_ALL"], 0) == massive.TIMING_ALL == (1 << len(massive.TIMING_GROUPS)) - 1
-    for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE"):
+    for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE", "SCORES_BY_RANK", "SCORES_BY_GID"):
         assert int(defs["MASSIVE_" + name]) == getattr(massive, name), name
 
 

@@ -70,6 +70,38 @@ def select_replacements(S_A_by_rank, h_of_rank, k):
     return [h for _, h in lsd_sort(lt)] + eq[:need]
 
 
+def select_replacements_by_gid(S_A_by_gid, rank_g, h_of_rank, gid_of, k):
+    """The kernels' steps with S_A over every global id, scanned in id order:
+    an exact radix select over the 64-bit key (~bits(S_A), rank), 8 bits a
+    pass (four on the score word, four on the rank word), then the k' keys
+    at or below it, in id order, stably sorted by rank and then by score."""
+    cands = [((~f32_bits(a)) & 0xFFFFFFFF, rank_g[g]) for g, a in enumerate(S_A_by_gid) if a >= 0.0]
+    need, pre, msk = k, [0, 0], [0, 0]
+    if k > 0:
+        for word in (0, 1):
+            for shift in (24, 16, 8, 0):
+                hist = [0] * 256
+                for c in cands:
+                    if (c[0] & msk[0]) == pre[0] and (c[1] & msk[1]) == pre[1]:
+                        hist[(c[word] >> shift) & 255] += 1
+                ex, pick, before = 0, -1, 0
+                for d in range(256):
+                    if ex < need <= ex + hist[d]:
+                        pick, before = d, ex
+                    ex += hist[d]
+                assert pick >= 0, "fewer candidates than asked for"
+                need -= before
+                pre[word] |= pick << shift
+                msk[word] |= 255 << shift
+        assert need == 1, "ranks are unique: one key at the threshold"
+    T = (pre[0], pre[1])  # the k'-th smallest key
+    emitted = [(c[1], h_of_rank[c[1]]) for c in cands if k > 0 and c <= T]
+    assert len(emitted) == k
+    by_rank = lsd_sort(emitted)
+    keyed = [((~f32_bits(S_A_by_gid[gid_of[h]])) & 0xFFFFFFFF, h) for _, h in by_rank] if by_rank else []
+    return [h for _, h in lsd_sort(keyed)]
+
+
 def narrow_evictions(E, S_E, rank_of_slot, k):
     """The kernels' steps: two stable sorts (rank, then S_E bits), keep k, sort by slot."""
     pairs = lsd_sort([(rank_of_slot[s], s) for s in E])
@@ -135,3 +167,29 @@ def test_eviction_narrowing_matches_sort(seed):
     for k in sorted({0, 1, len(E) // 2, len(E)}):
         want = sorted(sorted(E, key=lambda s: (S_E[s], rank_of_slot[s]))[:k])
         assert narrow_evictions(E, S_E, rank_of_slot, k) == want, (seed, cap, k)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_replacement_select_by_global_id_matches_sort(seed):
+    # S_A over a global id space larger than the halo (non-halo ids hold -1),
+    # halo nodes at random ids: the same replacements, in the same order, as
+    # the rank-ordered layout and a plain sort by (S_A desc, rank asc)
+    rnd = random.Random(100 + seed)
+    H = rnd.choice([1, 7, 300, 2500])
+    n_global = H + rnd.choice([0, 5, 3 * H])
+    gid_of = rnd.sample(range(n_global), H)          # halo h -> its global id
+    h_of_rank = list(range(H))
+    rnd.shuffle(h_of_rank)
+    S_by_rank = score_mix(rnd, H)
+    for r in rnd.sample(range(H), rnd.randrange(0, H)):
+        S_by_rank[r] = -1.0
+    S_by_gid, rank_g = [-1.0] * n_global, [-1] * n_global
+    for r, h in enumerate(h_of_rank):
+        S_by_gid[gid_of[h]] = S_by_rank[r]
+        rank_g[gid_of[h]] = r
+    ncand = sum(a >= 0.0 for a in S_by_rank)
+    for k in sorted({0, 1, ncand // 3, ncand // 2, max(ncand - 1, 0), ncand}):
+        want = [h_of_rank[r] for r in sorted((r for r in range(H) if S_by_rank[r] >= 0.0),
+                                             key=lambda r: (-S_by_rank[r], r))][:k]
+        assert select_replacements_by_gid(S_by_gid, rank_g, h_of_rank, gid_of, k) == want, (seed, H, k)
+        assert select_replacements(S_by_rank, h_of_rank, k) == want
