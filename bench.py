@@ -79,6 +79,56 @@ def build_inputs(w, threads=None):
     return g, local, store, sched
 
 
+def save_inputs(w, g, local, store, d):
+    """The inputs of a workload written once under d (/dev/shm), for child
+    processes that map them instead of generating the graph again."""
+    os.makedirs(d, exist_ok=True)
+    for name, arr in (("indptr", g.indptr), ("indices", g.indices), ("halo_gid", g.halo_gid),
+                      ("halo_degree", g.halo_degree), ("local", local), ("store", store.numpy()[:max(g.H, 1)])):
+        np.save(os.path.join(d, name + ".npy"), arr)
+    json.dump({"workload": w.name, "L": int(g.L), "H": int(g.H)}, open(os.path.join(d, "meta.json"), "w"))
+
+
+def load_inputs(w, d):
+    """A child's view of the inputs saved by save_inputs: the graph arrays
+    memory-mapped, the halo store copied into pinned memory."""
+    import types
+    import torch
+    import synth
+    meta = json.load(open(os.path.join(d, "meta.json")))
+    assert meta["workload"] == w.name, (meta, w.name)
+    m = {k: np.load(os.path.join(d, k + ".npy"), mmap_mode="r")
+         for k in ("indptr", "indices", "halo_gid", "halo_degree", "local", "store")}
+    g = types.SimpleNamespace(L=meta["L"], H=meta["H"], indptr=m["indptr"], indices=m["indices"],
+                              halo_gid=m["halo_gid"], halo_degree=m["halo_degree"], nnz=int(m["indices"].shape[0]))
+    store = torch.empty(m["store"].shape, dtype=torch.uint8, pin_memory=True)
+    store.numpy()[:] = m["store"]
+    sched = synth.Schedule(g.L, w.train_pct, w.batch, w.seed)
+    return g, np.asarray(m["local"]), store, sched
+
+
+class SharedInputs:
+    """A /dev/shm directory holding one workload's inputs for the children of
+    a parent process; removed when the parent leaves the with-block."""
+
+    def __init__(self, w, threads=None):
+        self.w, self.threads = w, threads
+        self.dir = "/dev/shm/massive_bench_%d" % os.getpid()
+
+    def __enter__(self):
+        g, local, store, _ = build_inputs(self.w, self.threads)
+        t0 = time.time()
+        save_inputs(self.w, g, local, store, self.dir)
+        log("inputs shared in %s (%.1fs)" % (self.dir, time.time() - t0))
+        del g, local, store
+        return self.dir
+
+    def __exit__(self, *exc):
+        import shutil
+        shutil.rmtree(self.dir, ignore_errors=True)
+        return False
+
+
 def window_plan(warmup, steps, delta, limit=20000):
     """The two timed windows of the default run, each [start, stop):
     early = the `steps` steps right after warm-up (before the first round when
@@ -483,6 +533,9 @@ def main():
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
                          "--copy-probe: the gather's HBM bytes over the headline window")
     ap.add_argument("--config-run", default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--inputs-dir", default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--sweep-point", nargs=4, default=None, metavar=("KIND", "F", "GAMMA", "DELTA"),
+                    help=argparse.SUPPRESS)
     ap.add_argument("--layouts", action="store_true",
                     help="the two S_A layouts of Section IV-B (over the halo in rank order, over every global "
                          "id) on the same eviction run, each in its own process: device memory, round time, "
@@ -511,13 +564,6 @@ def main():
     if args.config_run:
         config_run(args.config_run.split(","), args)
         return
-    if args.compare and args.compare_mode is None:
-        compare([a for a in sys.argv[1:]])
-        return
-    if args.layouts:
-        layouts([a for a in sys.argv[1:] if a != "--layouts"])
-        return
-
     import synth
 
     w = synth.get(args.workload)
@@ -525,15 +571,31 @@ def main():
             if v is not None}
     if over:
         w = w.with_(**over)
-    g, local, store, sched = build_inputs(w, args.threads)
+    parent_argv = [a for a in sys.argv[1:] if a not in ("--compare", "--layouts", "--sweep")]
+    if args.compare and args.compare_mode is None:
+        with SharedInputs(w, args.threads) as d:
+            compare(parent_argv + ["--inputs-dir", d])
+        return
+    if args.layouts:
+        with SharedInputs(w, args.threads) as d:
+            layouts(parent_argv + ["--inputs-dir", d])
+        return
+    if args.sweep and args.sweep_point is None:
+        with SharedInputs(w, args.threads) as d:
+            sweep(w, args, parent_argv + ["--inputs-dir", d])
+        return
+    if args.inputs_dir:
+        g, local, store, sched = load_inputs(w, args.inputs_dir)
+    else:
+        g, local, store, sched = build_inputs(w, args.threads)
+    if args.sweep_point:
+        print(json.dumps(sweep_point(w, args, g, local, store, sched)), flush=True)
+        return
     if args.compare:
         print(json.dumps(compare_one(w, args.compare_mode, g, local, store, sched, args)), flush=True)
         return
     if args.layout_run:
         print(json.dumps(layout_one(w, args.layout_run, g, local, store, sched, args)), flush=True)
-        return
-    if args.sweep:
-        sweep(w, g, local, store, sched, args)
         return
     if args.overlap:
         overlap(w, g, local, store, sched, args)
@@ -771,7 +833,7 @@ def compare(argv):
     import subprocess
     outs = {}
     for name in COMPARE_MODES:
-        cmd = [sys.executable, os.path.abspath(__file__)] + argv + ["--compare-mode", name]
+        cmd = [sys.executable, os.path.abspath(__file__)] + argv + ["--compare", "--compare-mode", name]
         r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
         if r.returncode != 0:
             log("mode %s failed with status %d" % (name, r.returncode))
@@ -787,43 +849,61 @@ def compare(argv):
         print(json.dumps(out), flush=True)
 
 
-def sweep(w, g, local, store, sched, args):
-    """Section V-B's analysis of f, gamma and delta (Fig. 12-13) on one partition's share:
-    every point from a fresh context over the same steps and seed schedule,
-    against no buffer and against the static buffer of the same f."""
+def sweep_point(w, args, g, local, store, sched):
+    """One point of the sweep in this process: a fresh context over 8 + N
+    steps with every kernel group timed."""
+    kind, f, gamma, delta = args.sweep_point
     warm, steps = 8, args.sweep_steps
-    total = warm + steps
+    wm = w.with_(buffer_pct=int(f), gamma=float(gamma), delta=int(delta))
+    res = run_context(wm, g, local, store, sched, [("run", warm, warm + steps, True)])
+    sm = summarize(wm, res, "run")
+    st = res["stats"]
+    hr = st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)
+    win = [round(float(x.mean()), 4) for x in np.array_split(hr, max(1, (warm + steps) // 64))]
+    tim = res["windows"]["run"]["tim"]
+    return {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": kind,
+            "workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
+            "steps": steps, "warmup": warm, "value": sm["value"], "unit": "minibatches/s",
+            "hit_rate": sm["hit_rate"], "eviction_rounds": sm["eviction_rounds"],
+            "evicted_rows": sm["evicted_rows"], "remote_rows_per_step": sm["remote_rows_per_step"],
+            "evict_ms_per_round": round(tim["evict_round"][0] / max(tim["evict_round"][1], 1), 3),
+            "hit_rate_per_64_steps": win}
 
-    def point(kind, wm, base):
-        res = run_context(wm, g, local, store, sched, [("run", warm, total, True)])
-        sm = summarize(wm, res, "run")
-        st = res["stats"]
-        hr = st[:, 1] / np.maximum(st[:, 1] + st[:, 2], 1)
-        win = [round(float(x.mean()), 4) for x in np.array_split(hr, max(1, total // 64))]
-        tim = res["windows"]["run"]["tim"]
-        out = {"metric": "sampled+gathered minibatches/s; remote rows per step", "mode": kind,
-               "workload": wm.name, "buffer_pct": wm.buffer_pct, "gamma": wm.gamma, "delta": wm.delta,
-               "steps": steps, "warmup": warm, "value": sm["value"], "unit": "minibatches/s",
-               "hit_rate": sm["hit_rate"], "eviction_rounds": sm["eviction_rounds"],
-               "evicted_rows": sm["evicted_rows"],
-               "remote_rows_per_step": sm["remote_rows_per_step"],
-               "remote_rows_vs_no_buffer": round(sm["remote_rows_per_step"] / base["remote_rows_per_step"], 4)
-               if base else 1.0,
-               "speedup_vs_no_buffer": round(sm["value"] / base["value"], 4) if base else 1.0,
-               "evict_ms_per_round": round(tim["evict_round"][0] / max(tim["evict_round"][1], 1), 3),
-               "hit_rate_per_64_steps": win}
+
+def sweep(w, args, argv):
+    """Section V-B's analysis of f, gamma and delta (Fig. 12-13) on one
+    partition's share: every point in a process of its own (the inputs are
+    mapped from shared memory), from a fresh context over the same steps and
+    seed schedule, against no buffer and against the static buffer of the
+    same f."""
+    import subprocess
+    total = 8 + args.sweep_steps
+    base = None
+
+    def point(kind, f, gamma, delta):
+        nonlocal base
+        cmd = [sys.executable, os.path.abspath(__file__)] + argv + ["--sweep-point", kind, str(f), str(gamma),
+                                                                     str(delta)]
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            raise SystemExit("bench: sweep point %s %s %s %s failed with status %d" % (kind, f, gamma, delta,
+                                                                                        r.returncode))
+        out = json.loads([l for l in r.stdout.splitlines() if l.startswith("{")][-1])
+        if base is None:
+            base = out
+        out["remote_rows_vs_no_buffer"] = round(out["remote_rows_per_step"] / max(base["remote_rows_per_step"], 1e-9), 4)
+        out["speedup_vs_no_buffer"] = round(out["value"] / base["value"], 4)
         log("%-9s f=%2d%% gamma=%-6g delta=%-5d %8.1f mb/s  hit %.3f  remote rows %.0f (%.3f)  rounds %d" %
-            (kind, wm.buffer_pct, wm.gamma, wm.delta, sm["value"], sm["hit_rate"], sm["remote_rows_per_step"],
-             out["remote_rows_vs_no_buffer"], sm["eviction_rounds"]))
+            (kind, out["buffer_pct"], out["gamma"], out["delta"], out["value"], out["hit_rate"],
+             out["remote_rows_per_step"], out["remote_rows_vs_no_buffer"], out["eviction_rounds"]))
         print(json.dumps(out), flush=True)
-        return sm
 
-    base = point("no_buffer", w.with_(buffer_pct=0), None)
+    point("no_buffer", 0, w.gamma, w.delta)
     for f in (15, 25, 35, 50):
-        point("static", w.with_(buffer_pct=f, delta=total + 1), base)
+        point("static", f, w.gamma, total + 1)
         for gamma in (0.95, 0.995, 0.9995):
             for delta in (16, 32, 64, 128, 256, 512, 1024):
-                point("eviction", w.with_(buffer_pct=f, gamma=gamma, delta=delta), base)
+                point("eviction", f, gamma, delta)
 
 
 def overlap(w, g, local, store, sched, args):
