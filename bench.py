@@ -545,6 +545,7 @@ def main():
                     help="the paper's parameter grid (f in 15/25/35/50 %%, gamma in 0.95/0.995/0.9995, delta in "
                          "16..1024) on the same inputs, plus no buffer and one static run per f; one JSON line each")
     ap.add_argument("--sweep-steps", type=int, default=1032, help="timed steps per sweep point (after 8 warm-up)")
+    ap.add_argument("--sweep-f", default="15,25,35,50", help="buffer sizes f (percent) of the sweep")
     ap.add_argument("--overlap", action="store_true",
                     help="Alg. 1's look-ahead against a stand-in trainer on its own stream (Section IV-C): "
                          "path alone, trainer alone, serial and overlapped steps per trainer size")
@@ -572,6 +573,9 @@ def main():
     if over:
         w = w.with_(**over)
     parent_argv = [a for a in sys.argv[1:] if a not in ("--compare", "--layouts", "--sweep")]
+    if "--sweep-f" in parent_argv:  # the grid is the parent's business
+        i = parent_argv.index("--sweep-f")
+        del parent_argv[i:i + 2]
     if args.compare and args.compare_mode is None:
         with SharedInputs(w, args.threads) as d:
             compare(parent_argv + ["--inputs-dir", d])
@@ -899,7 +903,7 @@ def sweep(w, args, argv):
         print(json.dumps(out), flush=True)
 
     point("no_buffer", 0, w.gamma, w.delta)
-    for f in (15, 25, 35, 50):
+    for f in [int(x) for x in args.sweep_f.split(",") if x]:
         point("static", f, w.gamma, total + 1)
         for gamma in (0.95, 0.995, 0.9995):
             for delta in (16, 32, 64, 128, 256, 512, 1024):
