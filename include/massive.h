@@ -40,7 +40,9 @@
  *     S_E, slot's S_E := the replacement's last S_A, replacement's S_A := -1.
  *
  * Threading: calls on one context must not overlap. Different contexts are
- * independent. Every call returns a status; nothing throws across the ABI.
+ * independent. A context in MASSIVE_LINK_STAGED mode runs host threads of
+ * its own, which end in massive_destroy. Every call returns a status;
+ * nothing throws across the ABI.
  */
 #ifndef MASSIVE_H
 #define MASSIVE_H
@@ -66,6 +68,16 @@ extern "C" {
 #define MASSIVE_SCORES_BY_RANK 0 /* S_A over the H halo nodes, in rank order */
 #define MASSIVE_SCORES_BY_GID 1  /* S_A over all n_global global ids, indexed by id */
 #define MASSIVE_MAX_INFLIGHT 3 /* batches enqueued and not yet waited for */
+
+/* How rows cross the host link (massive_init_args.link_mode): the misses,
+ * hits on slots still refilling, and the replacement rows of Algorithm 2's
+ * merged fetch. Both modes give the same results. */
+#define MASSIVE_LINK_LOADS 0  /* kernels read the mapped pinned store */
+#define MASSIVE_LINK_STAGED 1 /* host threads gather the rows into pinned
+                                 staging memory, the DMA engines copy them to
+                                 the device and a kernel scatters them; no
+                                 kernel reads host memory, so kernels running
+                                 beside the path (a trainer) are not slowed */
 
 typedef struct massive_ctx massive_ctx;
 
@@ -97,6 +109,11 @@ typedef struct {
   int64_t n_global;           /* MASSIVE_SCORES_BY_GID: the global id space,
                                  every halo_gid in [0, n_global) and distinct,
                                  n_global <= 2^31; ignored otherwise         */
+  int32_t link_mode;          /* MASSIVE_LINK_LOADS (0, the default) or
+                                 MASSIVE_LINK_STAGED                          */
+  int32_t link_threads;       /* MASSIVE_LINK_STAGED: host threads gathering
+                                 rows, 1..64 (0: 8); the context starts them
+                                 and one more that feeds the copies          */
 } massive_init_args;
 
 /* Creates a context: uploads G_p and local features to HBM, ranks the halo,

@@ -465,6 +465,78 @@ __global__ __launch_bounds__(256) void k_refill(const int2* __restrict__ list, c
   }
 }
 
+// ------------------------------------------------------------ staged host link
+// In the staged link mode the rows that cross the host link are gathered by
+// host threads into pinned staging memory and moved by the DMA engines, so
+// no kernel reads the host store. These kernels hand the row ids to the host
+// and scatter the staged rows on the device.
+
+// The host rows (.y) of the first min(*count, cap) entries of an (x, y)
+// list, and that count, written into pinned host memory through its device
+// views; made visible to the host before the kernel ends.
+__global__ __launch_bounds__(256) void k_rows_out(const int2* __restrict__ list, const int64_t* __restrict__ count,
+                                                  int64_t cap, int32_t* h_rows, int64_t* h_count) {
+  const int64_t n = min(max(*count, (int64_t)0), cap);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    h_rows[i] = list[i].y;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *h_count = n;
+  __threadfence_system();
+}
+
+// Misses: staged row r (miss-list entry lo + r, r < n) goes to output row
+// list[lo + r].x, and into buffer slot wslot[lo + r] as well when that is
+// >= 0 (a hit on a slot whose refill has not landed).
+template <typename V, bool ONE>
+__global__ __launch_bounds__(256) void k_scatter_rows(const uint8_t* __restrict__ stage, const int2* __restrict__ list,
+                                                      const int32_t* __restrict__ wslot, int64_t lo, int64_t n,
+                                                      uint8_t* __restrict__ dst, uint8_t* __restrict__ buf, int64_t rb,
+                                                      uint32_t cpr, uint64_t magic) {
+  const uint64_t total = (uint64_t)n * cpr;
+  for (uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total;
+       c += (uint64_t)gridDim.x * blockDim.x) {
+    uint64_t r, off;
+    chunk_of<V, ONE>(c, cpr, magic, r, off);
+    const V v = *reinterpret_cast<const V*>(stage + r * rb + off);
+    const int2 e = list[lo + r];
+    const int32_t ws = wslot[lo + r];
+    __builtin_nontemporal_store(v, reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e.x * rb + off));
+    if (ws >= 0) *reinterpret_cast<V*>(buf + (uint64_t)(uint32_t)ws * rb + off) = v;
+  }
+}
+
+// Refill: staged row r (fill-list entry lo + r, r < n) goes into the slab
+// row fill[lo + r].x, G lanes per row, under the rules of k_refill: skipped
+// for an entry that k_swap flagged or a slot that has landed already, and
+// published after a release fence with landed[slot] = round_id.
+template <typename V>
+__global__ __launch_bounds__(256) void k_refill_scatter(const uint8_t* __restrict__ stage,
+                                                        const int2* __restrict__ fill, int64_t lo, int64_t n,
+                                                        uint8_t* __restrict__ dst, int64_t rb, uint32_t cpr,
+                                                        uint32_t G, int32_t L, int32_t* __restrict__ landed,
+                                                        int32_t round_id, Counters* __restrict__ ctr) {
+  const int lane = lane_id();
+  const int rpw = MS_WAVE / (int)G;
+  const int sub = lane / (int)G, cl = lane % (int)G;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / MS_WAVE;
+  const int64_t nwaves = (int64_t)gridDim.x * blockDim.x / MS_WAVE;
+  for (int64_t r = wave * rpw + sub; r - sub < n; r += nwaves * rpw) {
+    bool ok = r < n;
+    const int2 e = ok ? fill[lo + r] : make_int2(-1, -1);
+    ok = ok && e.x >= L && e.y >= 0;
+    if (ok) ok = __hip_atomic_load(&landed[e.x - L], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != round_id;
+    if (ok)
+      for (uint32_t ch = cl; ch < cpr; ch += G) {
+        const uint64_t off = (uint64_t)ch * sizeof(V);
+        *reinterpret_cast<V*>(dst + (uint64_t)(uint32_t)e.x * rb + off) =
+            *reinterpret_cast<const V*>(stage + (uint64_t)r * rb + off);
+      }
+    __threadfence();
+    const uint64_t copied = __ballot(ok && cl == 0);
+    if (ok && cl == 0) __hip_atomic_store(&landed[e.x - L], round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0 && copied) atomicAdd((unsigned long long*)&ctr->refilled, (unsigned long long)__popcll(copied));
+  }
+}
+
 // ------------------------------------------------------------ lazy decay
 // S_E[s] is multiplied by gamma once for every step in which slot s was not
 // hit since the last materialisation: `steps` steps elapsed, hitcnt[s] of

@@ -6,24 +6,34 @@
 // next step at once; eviction rounds and their refill copies run on a copy
 // stream (the refill chunks and the HBM gathers wait for each other, and the
 // next classify waits for a round).
+// In the staged link mode no kernel reads host memory: a worker thread of the
+// context gathers each step's host rows and each refill chunk's rows into a
+// pinned ring (with a pool of host threads), copies them with the DMA engines
+// on a link stream, and enqueues the scatter kernels and the step's
+// completion there.
 // All device memory is allocated in massive_init; the per-step calls do not
 // allocate.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cmath>
 #include <cstring>
+#include <deque>
+#include <exception>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/massive.h"
 #include "buffer_kernels.hpp"
 #include "common.hpp"
+#include "gather_pool.hpp"
 #include "sample_kernels.hpp"
 
 namespace {
@@ -107,6 +117,59 @@ struct massive_ctx {
   int32_t tau_iters = ms::kTauIters;    // threshold passes per row (0 makes every long row fail)
   // streams and events
   hipStream_t s_main = nullptr, s_miss = nullptr, s_copy = nullptr;
+  // Staged host link (MASSIVE_LINK_STAGED). The worker thread takes jobs in
+  // order: a step's tail (its host rows gathered, copied and scattered, then
+  // the completion kernel and ev_batch_done, all on s_link) or one refill
+  // chunk (gathered, copied, scattered; the round's last chunk records
+  // ev_fill_done). Its ring entries and pool belong to it alone; the job queue
+  // and its progress are shared under lmu.
+  struct LinkJob {
+    bool refill = false;
+    int slot = 0;
+    int64_t step = 0;
+    const int2* list = nullptr;     // a step: its miss list, write-through slots and output rows
+    const int32_t* wslot = nullptr;
+    uint8_t* feat = nullptr;
+    ms::StepSizes* sz = nullptr;
+    int32_t pend = -1;              // the completion kernel's landed round (-1: none)
+    int64_t nbK = 0;                // frontier bound
+    bool rows = false;              // the step has host rows (H > 0)
+    int32_t round_id = 0, chunk = 0, nchunks = 1;  // a refill chunk
+    int timing = 0;                 // timing groups on when the job was posted
+  };
+  static constexpr int kRing = 4;  // staging ring entries
+  int64_t ring_bytes = 8 << 20;     // bytes per entry (at least one row)
+  int link_mode = MASSIVE_LINK_LOADS;
+  int link_threads = 8;
+  hipStream_t s_link = nullptr;
+  const uint8_t* h_store = nullptr;   // host address of the pinned store
+  int32_t* h_rows[kSlots] = {};       // pinned [H]: host rows of each slot's miss list
+  int32_t* hd_rows[kSlots] = {};      //   (device views)
+  int32_t* h_fill_rows = nullptr;     // pinned [cap]: host rows of the fill list
+  int32_t* hd_fill_rows = nullptr;
+  int64_t* h_cnt = nullptr;           // pinned [kSlots + 1]: miss count by slot, then the fill count
+  int64_t* hd_cnt = nullptr;
+  uint8_t* h_ring = nullptr;          // pinned [kRing][ring_rows * rb]
+  uint8_t* d_ring = nullptr;          // device [kRing][ring_rows * rb]
+  int64_t ring_rows = 0;
+  hipEvent_t ev_rows_ready[kSlots] = {};  // a slot's host rows are in h_rows (side stream)
+  hipEvent_t ev_fill_ready = nullptr;     // the round's fill rows are in h_fill_rows (copy stream)
+  hipEvent_t ev_fill_done = nullptr;      // the last refill chunk's scatter (link stream)
+  hipEvent_t ev_ring[kRing] = {};         // each ring entry's last scatter
+  bool ring_used[kRing] = {};
+  int ring_next = 0;
+  ms::GatherPool* pool = nullptr;
+  std::thread worker;
+  std::mutex lmu;
+  std::condition_variable lcv;
+  std::deque<LinkJob> ljobs;
+  bool lstop = false, lbusy = false, lfailed = false;
+  std::string lerr;
+  int64_t tail_step = -1;        // last step whose tail the worker has enqueued
+  int32_t fill_done_round = 0;   // last round whose refill chunks it has all enqueued
+  std::vector<hipEvent_t> lev_pool;  // the worker's timing events
+  std::vector<TimedRange> lpending;
+  bool staged() const { return link_mode == MASSIVE_LINK_STAGED; }
   // per step slot (step t uses slot t % MASSIVE_MAX_INFLIGHT): classify done
   // (main), HBM gather done and miss gather + mailbox done (side)
   hipEvent_t ev_cls_done[kSlots] = {}, ev_hbm_done[kSlots] = {}, ev_batch_done[kSlots] = {};
@@ -243,15 +306,26 @@ struct massive_ctx {
   }
   void resolve_timing() {
     for (auto& r : pending) {
-      float ms = 0.f;
-      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
-        tms[r.group] += ms;
-        tcalls[r.group] += 1;
-      }
+      add_range(r);
       ev_pool.push_back(r.a);
       ev_pool.push_back(r.b);
     }
     pending.clear();
+    // the worker's ranges (its events go back to its own pool)
+    std::lock_guard<std::mutex> lk(lmu);
+    for (auto& r : lpending) {
+      add_range(r);
+      lev_pool.push_back(r.a);
+      lev_pool.push_back(r.b);
+    }
+    lpending.clear();
+  }
+  void add_range(const TimedRange& r) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      tms[r.group] += ms;
+      tcalls[r.group] += 1;
+    }
   }
 };
 
@@ -422,8 +496,263 @@ int launch_refill_chunks(massive_ctx* c, int count, hipEvent_t after) {
   return MASSIVE_OK;
 }
 
+// ------------------------------------------------------------ staged host link
+#define HW(call)                                                                     \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess) return std::string(#call) + ": " + hipGetErrorString(e_); \
+  } while (0)
+
+int vec_for(int64_t rb, uintptr_t al) {
+  if (rb % 16 == 0 && al % 16 == 0) return 16;
+  if (rb % 8 == 0 && al % 8 == 0) return 8;
+  return 4;
+}
+
+// A timing event pair of the worker for group g, or nullptrs when g was off
+// when the job was posted.
+void link_timing(massive_ctx* c, int timing, int g, hipEvent_t* a, hipEvent_t* b) {
+  *a = *b = nullptr;
+  if (!((timing >> g) & 1)) return;
+  std::lock_guard<std::mutex> lk(c->lmu);
+  for (hipEvent_t* e : {a, b}) {
+    if (!c->lev_pool.empty()) {
+      *e = c->lev_pool.back();
+      c->lev_pool.pop_back();
+    } else if (hipEventCreate(e) != hipSuccess) {
+      *e = nullptr;
+    }
+  }
+  if (!*a || !*b) {
+    for (hipEvent_t e : {*a, *b})
+      if (e) c->lev_pool.push_back(e);
+    *a = *b = nullptr;
+  }
+}
+
+void link_timing_end(massive_ctx* c, hipEvent_t a, hipEvent_t b, int g) {
+  std::lock_guard<std::mutex> lk(c->lmu);
+  c->lpending.push_back({a, b, g});
+}
+
+// Store rows rows[0..n) through the ring, ring_rows at a time: an entry is
+// gathered on the host once its last scatter has run, copied to the device on
+// the link stream, then handed to scatter(stage, lo, m), which enqueues the
+// kernel that consumes staged rows lo..lo+m.
+template <class F>
+std::string link_rows(massive_ctx* c, const int32_t* rows, int64_t n, F&& scatter) {
+  hipStream_t s = c->s_link;
+  const int64_t eb = c->ring_rows * c->rb;
+  for (int64_t lo = 0; lo < n; lo += c->ring_rows) {
+    const int64_t m = std::min(c->ring_rows, n - lo);
+    const int e = c->ring_next;
+    c->ring_next = (e + 1) % massive_ctx::kRing;
+    if (c->ring_used[e]) HW(hipEventSynchronize(c->ev_ring[e]));
+    uint8_t* h = c->h_ring + e * eb;
+    uint8_t* d = c->d_ring + e * eb;
+    c->pool->gather(c->h_store, c->H, c->rb, rows + lo, m, h);
+    HW(hipMemcpyAsync(d, h, (size_t)(m * c->rb), hipMemcpyHostToDevice, s));
+    scatter(d, lo, m);
+    HW(hipGetLastError());
+    HW(hipEventRecord(c->ev_ring[e], s));
+    c->ring_used[e] = true;
+  }
+  return std::string();
+}
+
+template <typename V>
+void scatter_rows(hipStream_t s, const massive_ctx::LinkJob& j, const uint8_t* st, int64_t lo, int64_t m,
+                  uint8_t* buf, int64_t rb, uint32_t cpr, uint64_t magic) {
+  const unsigned grid = grid_for(m * cpr, 256, 4096);
+  if (cpr == 1)
+    ms::k_scatter_rows<V, true><<<grid, 256, 0, s>>>(st, j.list, j.wslot, lo, m, j.feat, buf, rb, cpr, magic);
+  else
+    ms::k_scatter_rows<V, false><<<grid, 256, 0, s>>>(st, j.list, j.wslot, lo, m, j.feat, buf, rb, cpr, magic);
+}
+
+template <typename V>
+void refill_scatter(massive_ctx* c, hipStream_t s, const uint8_t* st, int64_t lo, int64_t m, uint32_t cpr,
+                    uint32_t G, int32_t round_id) {
+  const int rows_per_block = (256 / MS_WAVE) * (MS_WAVE / (int)G);
+  const unsigned grid = grid_for(m, rows_per_block, 4096);
+  ms::k_refill_scatter<V><<<grid, 256, 0, s>>>(st, c->d_fill, lo, m, c->d_slab, c->rb, cpr, G, c->L, c->d_landed,
+                                              round_id, c->d_ctr);
+}
+
+// A step's tail: its host rows (misses and hits on refilling slots) through
+// the ring into their output rows (and write-through slots), then, after the
+// step's HBM gather, the completion kernel and the batch's event.
+std::string link_step(massive_ctx* c, const massive_ctx::LinkJob& j) {
+  hipStream_t s = c->s_link;
+  int64_t n = 0;
+  if (j.rows) {
+    HW(hipEventSynchronize(c->ev_rows_ready[j.slot]));
+    n = std::min<int64_t>(std::max<int64_t>(c->h_cnt[j.slot], 0), c->H);
+  }
+  if (n > 0) {
+    hipEvent_t ta, tb;
+    link_timing(c, j.timing, 3, &ta, &tb);
+    if (ta) HW(hipEventRecord(ta, s));
+    const int64_t rb = c->rb;
+    uint8_t* buf = c->d_slab + (int64_t)c->L * rb;
+    const int vec = vec_for(rb, (uintptr_t)j.feat | (uintptr_t)buf | (uintptr_t)c->d_ring);
+    const uint32_t cpr = (uint32_t)(rb / vec);
+    const uint64_t magic = cpr > 1 ? (~0ull) / cpr + 1 : 0;
+    std::string e = link_rows(c, c->h_rows[j.slot], n, [&](const uint8_t* st, int64_t lo, int64_t m) {
+      if (vec == 16)
+        scatter_rows<ms::v4u>(s, j, st, lo, m, buf, rb, cpr, magic);
+      else if (vec == 8)
+        scatter_rows<ms::v2u>(s, j, st, lo, m, buf, rb, cpr, magic);
+      else
+        scatter_rows<unsigned int>(s, j, st, lo, m, buf, rb, cpr, magic);
+    });
+    if (!e.empty()) return e;
+    if (ta) {
+      HW(hipEventRecord(tb, s));
+      link_timing_end(c, ta, tb, 3);
+    }
+  }
+  HW(hipStreamWaitEvent(s, c->ev_hbm_done[j.slot], 0));
+  const bool publish = j.pend >= 0;
+  ms::k_step_done<<<publish ? grid_for(j.nbK, 256, 1024) : 1, 256, 0, s>>>(
+      j.wslot, &j.sz->n_miss, c->d_landed, c->cap, j.pend, j.sz, c->K, &c->d_ctr->bad, c->hd_sz + j.slot,
+      c->hd_bad + j.slot);
+  HW(hipGetLastError());
+  HW(hipEventRecord(c->ev_batch_done[j.slot], s));
+  return std::string();
+}
+
+// One refill chunk of the current round: fill-list entries of the chunk
+// through the ring into their slots; the round's last chunk records
+// ev_fill_done.
+std::string link_refill(massive_ctx* c, const massive_ctx::LinkJob& j) {
+  hipStream_t s = c->s_link;
+  HW(hipEventSynchronize(c->ev_fill_ready));
+  const int64_t k = std::min<int64_t>(std::max<int64_t>(c->h_cnt[kSlots], 0), c->cap);
+  const int64_t lo = k * j.chunk / j.nchunks, hi = k * (j.chunk + 1) / j.nchunks;
+  if (hi > lo) {
+    hipEvent_t ta, tb;
+    link_timing(c, j.timing, 5, &ta, &tb);
+    if (ta) HW(hipEventRecord(ta, s));
+    const int vec = vec_for(c->rb, (uintptr_t)c->d_slab | (uintptr_t)c->d_ring);
+    const uint32_t cpr = (uint32_t)(c->rb / vec);
+    uint32_t G = 1;
+    while (G < cpr && G < MS_WAVE) G <<= 1;
+    std::string e = link_rows(c, c->h_fill_rows + lo, hi - lo, [&](const uint8_t* st, int64_t off, int64_t m) {
+      if (vec == 16)
+        refill_scatter<ms::v4u>(c, s, st, lo + off, m, cpr, G, j.round_id);
+      else if (vec == 8)
+        refill_scatter<ms::v2u>(c, s, st, lo + off, m, cpr, G, j.round_id);
+      else
+        refill_scatter<unsigned int>(c, s, st, lo + off, m, cpr, G, j.round_id);
+    });
+    if (!e.empty()) return e;
+    if (ta) {
+      HW(hipEventRecord(tb, s));
+      link_timing_end(c, ta, tb, 5);
+    }
+  }
+  if (j.chunk == j.nchunks - 1) HW(hipEventRecord(c->ev_fill_done, s));
+  return std::string();
+}
+#undef HW
+
+// The worker: jobs in posting order until the context ends. After a failure
+// it takes the remaining jobs without running them, so that every wait for
+// its progress ends; the failure is reported by the next call that waits.
+void link_loop(massive_ctx* c) {
+  const hipError_t de = hipSetDevice(c->device);
+  for (;;) {
+    massive_ctx::LinkJob j;
+    bool skip;
+    {
+      std::unique_lock<std::mutex> lk(c->lmu);
+      c->lcv.wait(lk, [c] { return c->lstop || !c->ljobs.empty(); });
+      if (c->ljobs.empty()) return;  // stopped, every job taken
+      j = c->ljobs.front();
+      c->ljobs.pop_front();
+      c->lbusy = true;
+      skip = c->lfailed;
+    }
+    std::string err;
+    if (de != hipSuccess)
+      err = std::string("hipSetDevice: ") + hipGetErrorString(de);
+    else if (!skip)
+      err = j.refill ? link_refill(c, j) : link_step(c, j);
+    {
+      std::lock_guard<std::mutex> lk(c->lmu);
+      if (!err.empty() && !c->lfailed) {
+        c->lfailed = true;
+        c->lerr = err;
+      }
+      if (!j.refill)
+        c->tail_step = j.step;
+      else if (j.chunk == j.nchunks - 1)
+        c->fill_done_round = j.round_id;
+      c->lbusy = false;
+    }
+    c->lcv.notify_all();
+  }
+}
+
+void link_post(massive_ctx* c, const massive_ctx::LinkJob& j) {
+  {
+    std::lock_guard<std::mutex> lk(c->lmu);
+    c->ljobs.push_back(j);
+  }
+  c->lcv.notify_all();
+}
+
+// Waits until done() holds (under the worker's lock) or the worker has failed.
+template <class P>
+int link_wait(massive_ctx* c, P done) {
+  std::string e;
+  {
+    std::unique_lock<std::mutex> lk(c->lmu);
+    c->lcv.wait(lk, [&] { return c->lfailed || done(); });
+    if (!c->lfailed) return MASSIVE_OK;
+    e = c->lerr;
+  }
+  c->broken = true;
+  return c->fail(MASSIVE_EHIP, "host-link worker: %s", e.c_str());
+}
+
+// Every posted job enqueued and the link stream idle (nothing to do in the
+// loads mode).
+int link_drain(massive_ctx* c) {
+  if (!c->staged()) return MASSIVE_OK;
+  const int rc = link_wait(c, [c] { return c->ljobs.empty() && !c->lbusy; });
+  if (rc != MASSIVE_OK) return rc;
+  CK(hipStreamSynchronize(c->s_link));
+  return MASSIVE_OK;
+}
+
+// Posts the next `count` refill chunks of the current round.
+void link_post_chunks(massive_ctx* c, int count) {
+  while (count-- > 0 && c->chunks_left > 0) {
+    massive_ctx::LinkJob j;
+    j.refill = true;
+    j.round_id = c->round_id;
+    j.chunk = c->refill_chunks - c->chunks_left;
+    j.nchunks = c->refill_chunks;
+    j.timing = c->timing;
+    link_post(c, j);
+    c->chunks_left -= 1;
+  }
+}
+
 void free_ctx(massive_ctx* c) {
   if (!c) return;
+  // the worker finishes the jobs already posted, then ends
+  if (c->worker.joinable()) {
+    {
+      std::lock_guard<std::mutex> lk(c->lmu);
+      c->lstop = true;
+    }
+    c->lcv.notify_all();
+    c->worker.join();
+  }
+  delete c->pool;
   (void)hipDeviceSynchronize();
   void* dev[] = {c->d_indptr, c->d_indices, c->d_slab, c->d_slot_id, c->d_S_E, c->d_hitcnt, c->d_S_A,
                  c->d_rank_of, c->d_h_of_rank, c->d_tab, c->d_pos_of, c->d_bits, c->d_sz, c->d_rs,
@@ -441,8 +770,23 @@ void free_ctx(massive_ctx* c) {
   if (c->h_bad) (void)hipHostFree(c->h_bad);
   if (c->h_ctr) (void)hipHostFree(c->h_ctr);
   for (int i = 0; i < kSlots; ++i)
-    for (hipEvent_t e : {c->ev_cls_done[i], c->ev_hbm_done[i], c->ev_batch_done[i], c->ev_miss_done[i]})
+    if (c->h_rows[i]) (void)hipHostFree(c->h_rows[i]);
+  for (void* p : {(void*)c->h_fill_rows, (void*)c->h_cnt, (void*)c->h_ring})
+    if (p) (void)hipHostFree(p);
+  if (c->d_ring) (void)hipFree(c->d_ring);
+  for (int i = 0; i < kSlots; ++i)
+    for (hipEvent_t e : {c->ev_cls_done[i], c->ev_hbm_done[i], c->ev_batch_done[i], c->ev_miss_done[i],
+                         c->ev_rows_ready[i]})
       if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->ev_ring)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : {c->ev_fill_ready, c->ev_fill_done})
+    if (e) (void)hipEventDestroy(e);
+  for (auto& r : c->lpending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : c->lev_pool) (void)hipEventDestroy(e);
   for (hipEvent_t e : {c->ev_round_done, c->ev_refill_done})
     if (e) (void)hipEventDestroy(e);
   for (auto& r : c->pending) {
@@ -452,6 +796,7 @@ void free_ctx(massive_ctx* c) {
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->s_miss) (void)hipStreamDestroy(c->s_miss);
   if (c->s_copy) (void)hipStreamDestroy(c->s_copy);
+  if (c->s_link) (void)hipStreamDestroy(c->s_link);
   delete c;
 }
 
@@ -503,7 +848,10 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (const char* e = getenv("MASSIVE_BIG_ROW")) c->big_min = std::max<int64_t>(256, atoll(e));
   if (const char* e = getenv("MASSIVE_BIG_BLOCKS")) c->big_blocks = std::max<int64_t>(1, atoll(e));
   if (const char* e = getenv("MASSIVE_TAU_ITERS")) c->tau_iters = std::min(std::max(0, atoi(e)), ms::kTauIters);
+  if (const char* e = getenv("MASSIVE_RING_BYTES")) c->ring_bytes = std::max<int64_t>(1, atoll(e));
   c->s_main = (hipStream_t)a->stream;
+  c->link_mode = a->link_mode;
+  c->link_threads = a->link_threads > 0 ? a->link_threads : 8;
   CK(hipGetDevice(&c->device));
   if (c->device < 0 || c->device >= kMaxDevices) return c->fail(MASSIVE_EHIP, "device %d out of range", c->device);
   {
@@ -518,6 +866,12 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
       CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
   for (hipEvent_t* e : {&c->ev_round_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+  if (c->staged()) {
+    CK(hipStreamCreateWithFlags(&c->s_link, hipStreamNonBlocking));
+    for (int i = 0; i < kSlots; ++i) CK(hipEventCreateWithFlags(&c->ev_rows_ready[i], hipEventDisableTiming));
+    for (hipEvent_t* e : {&c->ev_fill_ready, &c->ev_fill_done}) CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    for (hipEvent_t& e : c->ev_ring) CK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
 
   // the pinned store must be mapped into the device address space
   {
@@ -585,6 +939,30 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   if (hipHostGetDevicePointer((void**)&c->hd_sz, c->h_sz, 0) != hipSuccess || !c->hd_sz ||
       hipHostGetDevicePointer((void**)&c->hd_bad, c->h_bad, 0) != hipSuccess || !c->hd_bad)
     return c->fail(MASSIVE_EHIP, "the size mailboxes have no device view");
+  if (c->staged()) {
+    // host rows of each slot's misses (at most H per step), of a round's fill
+    // list (at most cap), their counts, and the staging ring
+    c->h_store = static_cast<const uint8_t*>(a->halo_store);
+    c->ring_rows = std::max<int64_t>(1, c->ring_bytes / rb);
+    const int64_t ring_bytes = massive_ctx::kRing * c->ring_rows * rb;
+    auto pinned = [](void** p, int64_t bytes) {
+      return hipHostMalloc(p, (size_t)std::max<int64_t>(bytes, 16), hipHostMallocDefault) == hipSuccess;
+    };
+    bool ok = true;
+    for (int i = 0; i < kSlots; ++i) ok = ok && pinned((void**)&c->h_rows[i], H * 4);
+    ok = ok && pinned((void**)&c->h_fill_rows, cap * 4) && pinned((void**)&c->h_cnt, (kSlots + 1) * 8) &&
+         pinned((void**)&c->h_ring, ring_bytes);
+    if (!ok) return c->fail(MASSIVE_ENOMEM, "hipHostMalloc of the staged link's buffers failed");
+    for (int i = 0; i < kSlots; ++i)
+      ok = ok && hipHostGetDevicePointer((void**)&c->hd_rows[i], c->h_rows[i], 0) == hipSuccess && c->hd_rows[i];
+    ok = ok && hipHostGetDevicePointer((void**)&c->hd_fill_rows, c->h_fill_rows, 0) == hipSuccess &&
+         c->hd_fill_rows && hipHostGetDevicePointer((void**)&c->hd_cnt, c->h_cnt, 0) == hipSuccess && c->hd_cnt;
+    if (!ok) return c->fail(MASSIVE_EHIP, "the staged link's row lists have no device view");
+    std::memset(c->h_cnt, 0, (kSlots + 1) * 8);
+    CKA(c->d_ring, ring_bytes);
+    c->pool = new ms::GatherPool(c->link_threads);
+    c->worker = std::thread(link_loop, c);
+  }
 
   hipStream_t s = c->s_main;
   CK(hipMemcpyAsync(c->d_indptr, a->indptr, (R + 1) * 8, hipMemcpyHostToDevice, s));
@@ -697,11 +1075,19 @@ int massive_init(const massive_init_args* a, massive_ctx** out) {
     for (int32_t h = 0; h < a->H; ++h)
       if (a->halo_gid[h] < 0 || a->halo_gid[h] >= a->n_global) return bad("a halo_gid lies outside [0, n_global)");
   }
+  if (a->link_mode != MASSIVE_LINK_LOADS && a->link_mode != MASSIVE_LINK_STAGED)
+    return bad("link_mode must be MASSIVE_LINK_LOADS or MASSIVE_LINK_STAGED");
+  if (a->link_threads < 0 || a->link_threads > 64) return bad("link_threads must be in 0..64");
   const int64_t R = (int64_t)a->L + a->H;
   if (a->indptr[0] != 0 || a->indptr[R] < 0) return bad("indptr must start at 0");
   massive_ctx* c = new (std::nothrow) massive_ctx();
   if (!c) return bad("out of host memory");
-  int rc = init_impl(c, a);
+  int rc;
+  try {
+    rc = init_impl(c, a);
+  } catch (const std::exception& e) {  // host threads or memory of the staged link
+    rc = c->fail(MASSIVE_ENOMEM, "massive_init: %s", e.what());
+  }
   if (rc != MASSIVE_OK) {
     g_init_error = c->err;
     free_ctx(c);
@@ -870,7 +1256,21 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   // A refill that may still be in flight: hits on its slots read the host
   // store instead (same bytes); once it has landed the buffer serves them.
   int32_t pend = -1;
-  if (c->round_pending_rows) {
+  if (c->round_pending_rows && c->staged()) {
+    // the worker has enqueued the round's last chunk and that has run
+    bool enq = false;
+    if (c->chunks_left == 0) {
+      std::lock_guard<std::mutex> lk(c->lmu);
+      enq = c->fill_done_round == c->round_id && !c->lfailed;
+    }
+    if (enq && hipEventQuery(c->ev_fill_done) == hipSuccess) {
+      c->round_pending_rows = false;
+      CK(hipStreamWaitEvent(s, c->ev_fill_done, 0));
+    } else {
+      (void)hipGetLastError();
+      pend = c->round_id;
+    }
+  } else if (c->round_pending_rows) {
     if (c->chunks_left == 0 && (!c->refill_inflight || hipEventQuery(c->ev_refill_done) == hipSuccess)) {
       c->round_pending_rows = false;
       if (c->refill_inflight) CK(hipStreamWaitEvent(s, c->ev_refill_done, 0));
@@ -924,6 +1324,36 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   launch_gather(c, 2, kHbm, sm, sb.hbm_list, &sz->n_hbm, c->d_slab, (uint8_t*)io->feat, c->rb, nb[c->K],
                 c->hbm_blocks);
   CK(hipEventRecord(c->ev_hbm_done[slot], sm));
+  if (c->staged()) {
+    // the host rows go to the worker, which enqueues the rest of the step
+    // (and then one refill chunk) on the link stream
+    if (c->H > 0) {
+      ms::k_rows_out<<<grid_for(std::min<int64_t>(nb[c->K], c->H), 256, 1024), 256, 0, sm>>>(
+          miss_list, &sz->n_miss, c->H, c->hd_rows[slot], c->hd_cnt + slot);
+      CK(hipEventRecord(c->ev_rows_ready[slot], sm));
+    }
+    CK(hipGetLastError());
+    massive_ctx::LinkJob j;
+    j.slot = slot;
+    j.step = c->t;
+    j.list = miss_list;
+    j.wslot = sb.miss_slot;
+    j.feat = (uint8_t*)io->feat;
+    j.sz = sz;
+    j.pend = pend >= 0 && c->H > 0 ? pend : -1;
+    j.nbK = nb[c->K];
+    j.rows = c->H > 0;
+    j.timing = c->timing;
+    link_post(c, j);
+    link_post_chunks(c, 1);
+    c->infl[slot].io = io;
+    c->infl[slot].step = c->t;
+    c->infl[slot].seeds = seeds;
+    c->infl[slot].n0 = n0;
+    c->t += 1;
+    c->pending_round = true;
+    return MASSIVE_OK;
+  }
   {
     int rc = launch_refill_chunks(c, 1, c->ev_hbm_done[slot]);
     if (rc != MASSIVE_OK) return rc;
@@ -977,6 +1407,11 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   if (slot < 0) return c->fail(MASSIVE_EINVAL, "this batch is not in flight");
   const massive_ctx::InFlight f = c->infl[slot];
   c->infl[slot] = massive_ctx::InFlight();
+  if (c->staged()) {  // the worker has enqueued the tails of this step and the earlier ones
+    const int64_t st = f.step;
+    const int rc = link_wait(c, [c, st] { return c->tail_step >= st; });
+    if (rc != MASSIVE_OK) return rc;
+  }
   CK(hipEventSynchronize(c->ev_batch_done[slot]));
   // Steps issued before this one and still in flight decide whether it is
   // valid: a step that failed on the device skipped its dedup scan and its
@@ -1092,7 +1527,18 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   hipStream_t s = c->s_copy;
   const int64_t cap = c->cap, H = c->H;
   ms::RoundState* rs = c->d_rs;
-  {
+  if (c->staged()) {
+    // The previous round's refill has landed before this round reassigns
+    // slots and rewrites the fill list and its host rows: its chunks are
+    // posted, the worker has enqueued the last one, and the round waits for it.
+    link_post_chunks(c, c->chunks_left);
+    if (c->round_id > 0) {
+      const int32_t prev = c->round_id;
+      const int rc = link_wait(c, [c, prev] { return c->fill_done_round >= prev; });
+      if (rc != MASSIVE_OK) return rc;
+      CK(hipStreamWaitEvent(s, c->ev_fill_done, 0));
+    }
+  } else {
     int rc = launch_refill_chunks(c, c->chunks_left, nullptr);
     if (rc != MASSIVE_OK) return rc;
   }
@@ -1161,6 +1607,11 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     ms::k_fill_gated<uint64_t><<<grid_for(c->hcap, 256), 256, 0, s>>>(c->d_tab, c->hcap, ms::kEmpty, &rs->k);
     ms::k_hash_insert<<<grid_for(cap, 256), 256, 0, s>>>(c->d_tab, c->hmask, c->d_slot_id, cap, &rs->k);
   }
+  if (c->staged()) {  // the fill list's host rows, for the worker's refill chunks
+    ms::k_rows_out<<<grid_for(cap, 256, 1024), 256, 0, s>>>(c->d_fill, &rs->k, cap, c->hd_fill_rows,
+                                                            c->hd_cnt + kSlots);
+    CK(hipEventRecord(c->ev_fill_ready, s));
+  }
   if (k_out) {
     CK(hipMemcpyAsync(&c->h_rs->k, &rs->k, 8, hipMemcpyDeviceToHost, s));
     CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, s));
@@ -1169,8 +1620,10 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   c->round_unclassified = true;
   // the refill is copied in chunks after the next steps' HBM gathers; the last
   // step's miss gather may still write rows of the previous round's
-  // replacements into slots this round reassigns, so the new refill comes after it
-  CK(hipStreamWaitEvent(s, c->ev_miss_done[tl % kSlots], 0));
+  // replacements into slots this round reassigns, so the new refill comes after
+  // it (in the staged mode the link stream orders them: the worker enqueues
+  // the new chunks after that step's tail)
+  if (!c->staged()) CK(hipStreamWaitEvent(s, c->ev_miss_done[tl % kSlots], 0));
   c->chunks_left = c->refill_chunks;
   c->round_pending_rows = true;
   CK(hipGetLastError());
@@ -1187,6 +1640,10 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
 
 int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted, int64_t* refilled) {
   if (!c) return MASSIVE_EINVAL;
+  {
+    const int rc = link_drain(c);  // staged refill chunks posted so far
+    if (rc != MASSIVE_OK) return rc;
+  }
   CK(hipStreamSynchronize(c->s_copy));  // refill chunks launched so far
   CK(hipMemcpyAsync(c->h_ctr, c->d_ctr, sizeof(ms::Counters), hipMemcpyDeviceToHost, c->s_main));
   CK(hipStreamSynchronize(c->s_main));
@@ -1198,6 +1655,10 @@ int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted, int6
 
 int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, int64_t* t) {
   if (!c) return MASSIVE_EINVAL;
+  {
+    const int rc = link_drain(c);
+    if (rc != MASSIVE_OK) return rc;
+  }
   hipStream_t s = c->s_main;
   CK(hipStreamSynchronize(c->s_miss));
   if (c->round_unclassified) CK(hipStreamWaitEvent(s, c->ev_round_done, 0));
@@ -1222,7 +1683,11 @@ int massive_get_state(massive_ctx* c, int32_t* slot_id, float* S_E, float* S_A, 
 
 int massive_get_buffer_rows(massive_ctx* c, void* out) {
   if (!c || (!out && c->cap)) return MASSIVE_EINVAL;
-  {
+  if (c->staged()) {  // every chunk of the round, through the worker
+    link_post_chunks(c, c->chunks_left);
+    const int rc = link_drain(c);
+    if (rc != MASSIVE_OK) return rc;
+  } else {
     int rc = launch_refill_chunks(c, c->chunks_left, nullptr);
     if (rc != MASSIVE_OK) return rc;
   }
@@ -1245,6 +1710,10 @@ int massive_set_timing(massive_ctx* c, int groups) {
   if (!c) return MASSIVE_EINVAL;
   if (groups & ~MASSIVE_TIMING_ALL) return c->fail(MASSIVE_EINVAL, "timing groups 0x%x outside 0x%x", groups,
                                                    MASSIVE_TIMING_ALL);
+  {
+    const int rc = link_drain(c);
+    if (rc != MASSIVE_OK) return rc;
+  }
   CK(hipDeviceSynchronize());
   c->resolve_timing();
   c->timing = groups;
@@ -1257,6 +1726,10 @@ int massive_set_timing(massive_ctx* c, int groups) {
 
 int massive_get_timing(massive_ctx* c, double* out_ms, int64_t* out_calls) {
   if (!c) return MASSIVE_EINVAL;
+  {
+    const int rc = link_drain(c);
+    if (rc != MASSIVE_OK) return rc;
+  }
   CK(hipStreamSynchronize(c->s_main));
   CK(hipStreamSynchronize(c->s_miss));
   CK(hipStreamSynchronize(c->s_copy));

@@ -17,6 +17,7 @@ MAX_HOPS = 8
 
 OK, EINVAL, ECAPACITY, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
 SCORES_BY_RANK, SCORES_BY_GID = 0, 1  # S_A layouts (Section IV-B)
+LINK_LOADS, LINK_STAGED = 0, 1  # how rows cross the host link: kernel loads, or host gather + DMA copies
 MAX_INFLIGHT = 3  # batches enqueued with sample_async and not yet waited for
 _NAMES = {EINVAL: "EINVAL", ECAPACITY: "ECAPACITY", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE"}
 
@@ -40,7 +41,8 @@ class InitArgs(ctypes.Structure):
                 ("row_bytes", ctypes.c_int64), ("K", ctypes.c_int32),
                 ("fanout", ctypes.c_int32 * MAX_HOPS), ("buffer_pct", ctypes.c_int32),
                 ("gamma", ctypes.c_float), ("delta", ctypes.c_int32), ("seed", ctypes.c_uint64),
-                ("stream", ctypes.c_void_p), ("score_layout", ctypes.c_int32), ("n_global", ctypes.c_int64)]
+                ("stream", ctypes.c_void_p), ("score_layout", ctypes.c_int32), ("n_global", ctypes.c_int64),
+                ("link_mode", ctypes.c_int32), ("link_threads", ctypes.c_int32)]
 
 
 class Batch(ctypes.Structure):
@@ -147,9 +149,12 @@ class Massive:
 
     def __init__(self, L, H, indptr, indices, halo_gid, halo_degree, local_feat, halo_store,
                  row_bytes, fanout: Sequence[int], buffer_pct: int, gamma: float, delta: int,
-                 seed: int = 0, stream=None, score_layout: str = "rank", n_global: int = 0):
+                 seed: int = 0, stream=None, score_layout: str = "rank", n_global: int = 0,
+                 link: str = "loads", link_threads: int = 0):
         """score_layout: "rank" (S_A over the halo, in rank order) or "gid"
-        (S_A over all n_global global ids)."""
+        (S_A over all n_global global ids). link: "loads" (kernels read the
+        pinned store) or "staged" (link_threads host threads gather the rows,
+        0 for the library's default, and the DMA engines copy them)."""
         import torch
         self._torch = torch
         self._lib = load()
@@ -192,7 +197,12 @@ class Massive:
             raise ValueError("score_layout must be 'rank' or 'gid'")
         a.score_layout = SCORES_BY_GID if score_layout == "gid" else SCORES_BY_RANK
         a.n_global = int(n_global)
+        if link not in ("loads", "staged"):
+            raise ValueError("link must be 'loads' or 'staged'")
+        a.link_mode = LINK_STAGED if link == "staged" else LINK_LOADS
+        a.link_threads = int(link_threads)
         self.score_layout = score_layout
+        self.link = link
         h = ctypes.c_void_p()
         rc = self._lib.massive_init(ctypes.byref(a), ctypes.byref(h))
         if rc != OK:

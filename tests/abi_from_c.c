@@ -30,6 +30,8 @@ int main(int argc, char** argv) {
   F(massive_init_args, stream);
   F(massive_init_args, score_layout);
   F(massive_init_args, n_global);
+  F(massive_init_args, link_mode);
+  F(massive_init_args, link_threads);
   printf("massive_init_args sizeof %zu 0\n", sizeof(massive_init_args));
   F(massive_batch, nodes);
   F(massive_batch, mask);

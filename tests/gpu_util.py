@@ -33,17 +33,19 @@ def pinned_store(prob: Problem):
 
 def make_gpu(prob: Problem, store=None, **over):
     """A context on prob; over may set fanout, buffer_pct, gamma, delta, seed,
-    and score_layout ("rank" or "gid", with n_global)."""
+    score_layout ("rank" or "gid", with n_global) and link ("loads" or
+    "staged", with link_threads)."""
     from paper_2410_22697_amd import Massive
     kw = dict(fanout=prob.fanout, buffer_pct=prob.buffer_pct, gamma=prob.gamma, delta=prob.delta, seed=prob.seed,
-              score_layout="rank", n_global=0)
+              score_layout="rank", n_global=0, link="loads", link_threads=0)
     kw.update(over)
     if store is None:
         store = pinned_store(prob)
     lf = np.ascontiguousarray(prob.local_feat).view(np.uint8).reshape(prob.L, prob.row_bytes)
     return Massive(prob.L, prob.H, prob.indptr, prob.indices, prob.halo_gid, prob.halo_degree, lf, store,
                    prob.row_bytes, kw["fanout"], kw["buffer_pct"], kw["gamma"], kw["delta"], kw["seed"],
-                   score_layout=kw["score_layout"], n_global=kw["n_global"])
+                   score_layout=kw["score_layout"], n_global=kw["n_global"], link=kw["link"],
+                   link_threads=kw["link_threads"])
 
 
 def to_dev(a):
@@ -118,3 +120,57 @@ def run_parity(name, prob: Problem, seeds_of, steps, state_every=1, buffer_rows_
     log("%s: %d steps, %d rounds, hit rate %.3f, %.1fs" % (name, steps, rounds, hits / max(hits + misses, 1),
                                                            time.time() - t0))
     return rounds, hits, misses
+
+
+def run_lookahead(name, prob, seeds_of, steps, depth=None, **over):
+    """Steps 0..steps-1 with `depth` batches in flight (step t is enqueued
+    before step t - depth + 1 is waited for), against the oracle step by
+    step; `over` goes to make_gpu. Returns (rounds, pending hits served over
+    the host link)."""
+    import torch
+    from paper_2410_22697_amd import MAX_INFLIGHT
+    depth = depth or MAX_INFLIGHT
+    orc = prob.oracle()
+    gm = make_gpu(prob, **over)
+    K = len(prob.fanout)
+    batch_max = max(len(seeds_of(t)) for t in range(steps))
+    bbs = [gm.alloc_batch(batch_max) for _ in range(depth)]
+    cap = gm.cap
+    outs = [tuple(torch.full((max(cap, 1),), -7, dtype=torch.int32, device="cuda") for _ in range(3))
+            for _ in range(steps)]
+    seeds_dev = [to_dev(seeds_of(t)) for t in range(steps)]
+    rounds_o, evicted_o = [], 0
+    pending = []
+
+    def check(t):
+        res = gm.wait(bbs[t % depth])
+        pending.append(res.host_rows - res.misses)
+        st = orc.sample(seeds_of(t))
+        compare_step("%s t=%d" % (name, t), st, res, bbs[t % depth], K)
+        ro = orc.evict_step()
+        rounds_o.append(ro)
+        return ro.k
+
+    for t in range(steps):
+        log("%s t=%d enqueue" % (name, t))
+        gm.sample_async(seeds_dev[t], bbs[t % depth])
+        gm.evict_step(outs[t], wait=False)
+        if t >= depth - 1:
+            evicted_o += check(t - depth + 1)
+    for t in range(max(0, steps - depth + 1), steps):
+        evicted_o += check(t)
+    torch.cuda.synchronize()
+    n_rounds = 0
+    for t, ro in enumerate(rounds_o):
+        if ro.k:
+            n_rounds += 1
+            ev, sl, rp = (x[:ro.k].cpu().numpy() for x in outs[t])
+            assert np.array_equal(sl, ro.slots) and np.array_equal(ev, ro.evicted) and np.array_equal(rp, ro.replaced), t
+    compare_state(name + " end", orc, gm)
+    assert np.array_equal(gm.buffer_rows(), orc.buffer_rows())
+    assert gm.counters() == (n_rounds, evicted_o)
+    # the refill copies each replacement at most once, and none a miss gather wrote through
+    assert cap <= gm.refilled_rows() <= cap + evicted_o
+    log("%s: %d steps, %d rounds, %d evicted, pending hits per step %s" % (name, steps, n_rounds, evicted_o, pending))
+    assert min(pending) >= 0
+    return n_rounds, sum(pending)

@@ -29,7 +29,8 @@ def test_binding_constants_match_the_header():
     assert int(defs["MASSIVE_MAX_HOPS"]) == massive.MAX_HOPS
     assert int(defs["MASSIVE_MAX_INFLIGHT"]) == massive.MAX_INFLIGHT
     assert int(defs["MASSIVE_TIMING_ALL"], 0) == massive.TIMING_ALL == (1 << len(massive.TIMING_GROUPS)) - 1
-    for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE", "SCORES_BY_RANK", "SCORES_BY_GID"):
+    for name in ("OK", "EINVAL", "ECAPACITY", "ENOMEM", "EHIP", "ESTATE", "SCORES_BY_RANK", "SCORES_BY_GID",
+                 "LINK_LOADS", "LINK_STAGED"):
         assert int(defs["MASSIVE_" + name]) == getattr(massive, name), name
 
 
@@ -62,7 +63,8 @@ _BAD = [("K", 0, b"K must"), ("K", 9, b"K must"), ("fanout0", 0, b"fanout"), ("f
         ("buffer_pct", 101, b"buffer_pct"), ("buffer_pct", -1, b"buffer_pct"), ("gamma", 0.0, b"gamma"),
         ("gamma", 1.5, b"gamma"), ("delta", 0, b"delta"), ("row_bytes", 6, b"row_bytes"),
         ("row_bytes", 0, b"row_bytes"), ("row_bytes", (1 << 20) + 4, b"row_bytes"),
-        ("L", -1, b"L >= 0")]
+        ("L", -1, b"L >= 0"), ("link_mode", 2, b"link_mode"), ("link_mode", -1, b"link_mode"),
+        ("link_threads", -1, b"link_threads"), ("link_threads", 65, b"link_threads")]
 
 
 @pytest.mark.parametrize("field,value,msg", _BAD)

@@ -8,7 +8,7 @@ skips them); the outputs and the buffer rows must not change."""
 import numpy as np
 import pytest
 
-from gpu_util import compare_state, compare_step, log, make_gpu, require_gpu, to_dev
+from gpu_util import compare_step, log, make_gpu, require_gpu, run_lookahead, to_dev
 from helpers import workload_problem
 
 pytestmark = pytest.mark.gpu
@@ -17,58 +17,6 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(autouse=True)
 def _gpu():
     require_gpu()
-
-
-def run_lookahead(name, prob, seeds_of, steps, depth=None):
-    """Steps 0..steps-1 with `depth` batches in flight (step t is enqueued
-    before step t - depth + 1 is waited for)."""
-    import torch
-    from paper_2410_22697_amd import MAX_INFLIGHT
-    depth = depth or MAX_INFLIGHT
-    orc = prob.oracle()
-    gm = make_gpu(prob)
-    K = len(prob.fanout)
-    batch_max = max(len(seeds_of(t)) for t in range(steps))
-    bbs = [gm.alloc_batch(batch_max) for _ in range(depth)]
-    cap = gm.cap
-    outs = [tuple(torch.full((max(cap, 1),), -7, dtype=torch.int32, device="cuda") for _ in range(3))
-            for _ in range(steps)]
-    seeds_dev = [to_dev(seeds_of(t)) for t in range(steps)]
-    rounds_o, evicted_o = [], 0
-    pending = []
-
-    def check(t):
-        res = gm.wait(bbs[t % depth])
-        pending.append(res.host_rows - res.misses)
-        st = orc.sample(seeds_of(t))
-        compare_step("%s t=%d" % (name, t), st, res, bbs[t % depth], K)
-        ro = orc.evict_step()
-        rounds_o.append(ro)
-        return ro.k
-
-    for t in range(steps):
-        log("%s t=%d enqueue" % (name, t))
-        gm.sample_async(seeds_dev[t], bbs[t % depth])
-        gm.evict_step(outs[t], wait=False)
-        if t >= depth - 1:
-            evicted_o += check(t - depth + 1)
-    for t in range(max(0, steps - depth + 1), steps):
-        evicted_o += check(t)
-    torch.cuda.synchronize()
-    n_rounds = 0
-    for t, ro in enumerate(rounds_o):
-        if ro.k:
-            n_rounds += 1
-            ev, sl, rp = (x[:ro.k].cpu().numpy() for x in outs[t])
-            assert np.array_equal(sl, ro.slots) and np.array_equal(ev, ro.evicted) and np.array_equal(rp, ro.replaced), t
-    compare_state(name + " end", orc, gm)
-    assert np.array_equal(gm.buffer_rows(), orc.buffer_rows())
-    assert gm.counters() == (n_rounds, evicted_o)
-    # the refill copies each replacement at most once, and none a miss gather wrote through
-    assert cap <= gm.refilled_rows() <= cap + evicted_o
-    log("%s: %d steps, %d rounds, %d evicted, pending hits per step %s" % (name, steps, n_rounds, evicted_o, pending))
-    assert min(pending) >= 0
-    return n_rounds, sum(pending)
 
 
 @pytest.mark.parametrize("depth", [2, 3])
