@@ -56,6 +56,8 @@ SAMPLER_STEPS = 16           # steps of the sampler measurement
 # those whose stated run ends before the first round
 CONFIG_GROUPS = (("cl10k", "cl170k"), ("cl2m45",), ("cl2m45_bf16",))
 EXTENDED_ROUNDS = 4
+# how rows cross the host link in every context of this process (--link)
+LINK = {"link": "loads", "link_threads": 0}
 
 
 def log(msg):
@@ -183,7 +185,7 @@ def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False,
     free0 = torch.cuda.mem_get_info()[0]
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
                  w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed, score_layout=score_layout,
-                 n_global=w.n)
+                 n_global=w.n, link=LINK["link"], link_threads=LINK["link_threads"])
     torch.cuda.synchronize()
     init_s = time.time() - t0
     ctx_bytes = free0 - torch.cuda.mem_get_info()[0]  # device memory the context holds
@@ -499,6 +501,7 @@ def configs_in_children(args):
             cmd.append("--no-cpu")
         if args.threads:
             cmd += ["--threads", str(args.threads)]
+        cmd += ["--link", args.link, "--link-threads", str(args.link_threads)]
         log("configs %s: %s" % (",".join(group), " ".join(cmd[1:])))
         r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
         if r.returncode != 0:
@@ -519,6 +522,10 @@ def main():
     ap.add_argument("--no-eviction-run", action="store_true", help="skip the eviction run and the sampler pass")
     ap.add_argument("--threads", type=int, default=None, help="host threads of the input generator")
     ap.add_argument("--log-steps", action="store_true", help="per-step row counts on stderr")
+    ap.add_argument("--link", choices=("loads", "staged"), default="loads",
+                    help="how rows cross the host link: kernel loads of the pinned store, or host threads "
+                         "gathering into pinned staging and DMA copies")
+    ap.add_argument("--link-threads", type=int, default=0, help="host gather threads of --link staged (0: default)")
     ap.add_argument("--depth", type=int, default=DEFAULT_DEPTH, help="batches in flight (1 to 3)")
     ap.add_argument("--delta", type=int, default=None, help="override the eviction interval")
     ap.add_argument("--gamma", type=float, default=None, help="override the decay factor")
@@ -559,6 +566,7 @@ def main():
         print("bench.py measures one GPU: the library has no multi-GPU path (each partition's "
               "buffer is private to its trainer); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    LINK.update(link=args.link, link_threads=args.link_threads)
     if args.pmc_summary:
         pmc_summary(args)
         return
@@ -666,7 +674,7 @@ def main():
                    "warmup_requested": args.warmup,
                    "window_rule": "the timed steps lie after the first eviction round and contain a round "
                                   "(centred on one when shorter than delta); the steps before them run untimed",
-                   "parallelism": "one partition on one GPU"},
+                   "parallelism": "one partition on one GPU", "link": LINK["link"]},
         "gather_GBps": g_["GBps"],
         "gather_frac_hbm": g_["frac_hbm"],
         "hit_rate": sm["hit_rate"],
@@ -923,7 +931,8 @@ def overlap(w, g, local, store, sched, args):
     assert w.dtype == "f32", "the stand-in trainer reads fp32 rows"
     torch.cuda.set_device(0)
     gm = Massive(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store, w.row_bytes,
-                 w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
+                 w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed, link=LINK["link"],
+                 link_threads=LINK["link_threads"])
     main = torch.cuda.current_stream()
     consumer = torch.cuda.Stream()
     bbs = [gm.alloc_batch(w.batch), gm.alloc_batch(w.batch)]
@@ -1014,7 +1023,7 @@ def overlap(w, g, local, store, sched, args):
         T_ovl = timed(lookahead, W, tr)
         eff = (t_prep + t_ddp - T_ovl) / min(t_prep, t_ddp)
         out = {"metric": "ms per minibatch, prepare overlapped with a stand-in trainer", "mode": "overlap",
-               "workload": w.name, "steps": W, "trainer": "2-layer MLP fwd+bwd fp32, hidden %d, %d rows" % (hid, n),
+               "workload": w.name, "steps": W, "link": LINK["link"], "trainer": "2-layer MLP fwd+bwd fp32, hidden %d, %d rows" % (hid, n),
                "t_prepare_ms": round(1e3 * t_prep, 4), "t_ddp_ms": round(1e3 * t_ddp, 4),
                "T_serial_ms": round(1e3 * T_ser, 4), "T_overlap_ms": round(1e3 * T_ovl, 4),
                "eq5_max_ms": round(1e3 * max(t_prep, t_ddp), 4),

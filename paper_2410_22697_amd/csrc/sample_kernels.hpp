@@ -310,8 +310,10 @@ struct PhiloxRow {
     a2hi = (uint32_t)(a2 >> 32);
     a2lo = (uint32_t)a2;
   }
-  __device__ __forceinline__ uint4 operator()(uint32_t q) const {
-    const uint64_t a1 = (uint64_t)0xD2511F53u * q;  // round 1, word 0
+  // the block of counter q, given round 1's product of word 0, a1 = M0 * q
+  // (a lane's consecutive iterations add M0 * 64 to it instead of
+  // multiplying again)
+  __device__ __forceinline__ uint4 from_a1(uint64_t a1) const {
     const uint32_t z1 = (uint32_t)(a1 >> 32) ^ hop ^ k1, w1 = (uint32_t)a1;
     uint32_t r0 = k0 + 0x9E3779B9u, r1 = k1 + 0xBB67AE85u;  // round 2's key
     const uint64_t b2 = (uint64_t)0xCD9E8D57u * z1;
@@ -422,41 +424,76 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// Appends to c (at cnt, in ascending j) the candidates (key << 32 | j) among
+// the four keys of block q = q0 + lane whose key is <= tm1, stopping at
+// kCandCap entries but counting them all. Every lane's four positions exist;
+// mn is the smallest of the lane's four keys.
+// A row's ~fanout + 3 sqrt(fanout) + 3 candidates are spread over its
+// iterations, so an iteration with a candidate usually has one, or a few in
+// different lanes: when no lane has two, a lane's candidate is its smallest
+// key and its list index the running count plus the candidate lanes below it.
+__device__ __forceinline__ void take_block(uint4 k4, uint32_t mn, uint32_t q, uint32_t tm1, uint64_t* c, int& cnt) {
+  pin(k4.x);
+  pin(k4.y);
+  pin(k4.z);
+  pin(k4.w);
+  const uint64_t m0 = ballot(k4.x <= tm1), m1 = ballot(k4.y <= tm1), m2 = ballot(k4.z <= tm1),
+                 m3 = ballot(k4.w <= tm1);
+  const uint64_t any = m0 | m1 | m2 | m3;
+  if (!any) return;
+  const uint64_t bit = 1ull << lane_id();
+  const int n_any = __popcll(any);
+  if (__popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3) == n_any) {  // one per candidate lane
+    if (any & bit) {
+      const uint32_t s = (m0 & bit) ? 0u : (m1 & bit) ? 1u : (m2 & bit) ? 2u : 3u;
+      const int p = cnt + lanes_below(any);
+      if (p < kCandCap) c[p] = ((uint64_t)mn << 32) | (4 * q + s);
+    }
+    cnt += n_any;
+    return;
+  }
+  // lower lanes first, then s within the lane
+  int p = cnt + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+  const uint64_t m[4] = {m0, m1, m2, m3};
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    if (m[s] & bit) {
+      if (p < kCandCap) c[p] = ((uint64_t)word_of(k4, s) << 32) | (4 * q + s);
+      ++p;
+    }
+  cnt += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+}
+
+__device__ __forceinline__ uint32_t min4(const uint4& w) { return min(min(w.x, w.y), min(w.z, w.w)); }
+
 // Filters 4-position groups [g0, g1) of a row of d positions: appends to c, in
 // ascending j, the candidates (key << 32 | j) whose key is <= tm1 (below tau),
 // stopping at kCandCap entries but counting them all. One wavefront.
+// The usual iteration of a long row has no key below tau, which one test on
+// the smallest of each lane's four keys settles. (Two or four Philox blocks
+// per lane in flight were measured slower: the loop is bound by VALU issue,
+// not by the latency of its dependent multiplies.)
 __device__ __forceinline__ int filter_groups(const PhiloxRow& ph, uint32_t g0, uint32_t g1, uint32_t d32,
                                              uint32_t tm1, uint64_t* c) {
   const int lane = lane_id();
   int cnt = 0;
-  for (uint32_t q0 = g0; q0 < g1; q0 += MS_WAVE) {
+  const uint32_t gf = min(g1, d32 / 4);  // groups below gf are whole
+  uint64_t a1 = (uint64_t)0xD2511F53u * (g0 + lane);
+  for (uint32_t q0 = g0; q0 < g1; q0 += MS_WAVE, a1 += (uint64_t)0xD2511F53u * MS_WAVE) {
     const uint32_t q = q0 + lane;
-    const uint4 wv = ph(q);
-    // lane masks of the keys below tau, position j = 4q + s (held as scalar
-    // masks: the usual iteration of a long row takes none)
-    uint64_t m0, m1, m2, m3;
-    if (q0 + MS_WAVE <= g1 && 4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
-      // one test on the smallest of the four keys first (the usual case:
-      // none below tau); the keys are pinned so the four tests stay behind it
-      if (!ballot(min(min(wv.x, wv.y), min(wv.z, wv.w)) <= tm1)) continue;
-      uint4 k4 = wv;
-      pin(k4.x);
-      pin(k4.y);
-      pin(k4.z);
-      pin(k4.w);
-      m0 = ballot(k4.x <= tm1);
-      m1 = ballot(k4.y <= tm1);
-      m2 = ballot(k4.z <= tm1);
-      m3 = ballot(k4.w <= tm1);
-    } else {
-      const bool in = q < g1;
-      m0 = ballot(in && 4 * q < d32 && wv.x <= tm1);
-      m1 = ballot(in && 4 * q + 1 < d32 && wv.y <= tm1);
-      m2 = ballot(in && 4 * q + 2 < d32 && wv.z <= tm1);
-      m3 = ballot(in && 4 * q + 3 < d32 && wv.w <= tm1);
+    const uint4 wv = ph.from_a1(a1);
+    if (q0 + MS_WAVE <= gf) {  // every position of this iteration exists
+      const uint32_t mn = min4(wv);
+      if (!ballot(mn <= tm1)) continue;
+      take_block(wv, mn, q, tm1, c, cnt);
+      continue;
     }
+    const bool in = q < g1;
+    const uint64_t m0 = ballot(in && 4 * q < d32 && wv.x <= tm1);
+    const uint64_t m1 = ballot(in && 4 * q + 1 < d32 && wv.y <= tm1);
+    const uint64_t m2 = ballot(in && 4 * q + 2 < d32 && wv.z <= tm1);
+    const uint64_t m3 = ballot(in && 4 * q + 3 < d32 && wv.w <= tm1);
     if (!(m0 | m1 | m2 | m3)) continue;
-    // candidates in ascending j: lower lanes first, then s within the lane
     int p = cnt + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
     const uint64_t bit = 1ull << lane;
     const uint64_t m[4] = {m0, m1, m2, m3};
@@ -506,46 +543,7 @@ __global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_waves(SampleAr
   const uint32_t d32 = (uint32_t)d;  // a row is shorter than 2^31
   const PhiloxRow ph((uint32_t)v, a.t, (uint32_t)a.hop, a.key0, a.key1);
   for (int iter = 0; iter < a.tau_iters && !fail; ++iter) {
-    cnt = 0;
-    const uint32_t tm1 = (uint32_t)(ts.tau - 1);  // key < tau  <=>  key <= tau - 1
-    for (uint32_t q0 = 0; 4 * q0 < d32; q0 += MS_WAVE) {
-      const uint32_t q = q0 + lane;
-      const uint4 wv = ph(q);
-      // lane masks of the keys below tau, position j = 4q + s (held as scalar
-      // masks: the usual iteration of a long row takes none)
-      uint64_t m0, m1, m2, m3;
-      if (4 * (q0 + MS_WAVE) <= d32) {  // every position of this iteration exists
-        // one test on the smallest of the four keys first (the usual case:
-        // none below tau); the keys are pinned so the four tests stay behind it
-        if (!ballot(min(min(wv.x, wv.y), min(wv.z, wv.w)) <= tm1)) continue;
-        uint4 k4 = wv;
-        pin(k4.x);
-        pin(k4.y);
-        pin(k4.z);
-        pin(k4.w);
-        m0 = ballot(k4.x <= tm1);
-        m1 = ballot(k4.y <= tm1);
-        m2 = ballot(k4.z <= tm1);
-        m3 = ballot(k4.w <= tm1);
-      } else {
-        m0 = ballot(4 * q < d32 && wv.x <= tm1);
-        m1 = ballot(4 * q + 1 < d32 && wv.y <= tm1);
-        m2 = ballot(4 * q + 2 < d32 && wv.z <= tm1);
-        m3 = ballot(4 * q + 3 < d32 && wv.w <= tm1);
-      }
-      if (!(m0 | m1 | m2 | m3)) continue;
-      // candidates in ascending j: lower lanes first, then s within the lane
-      int p = cnt + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
-      const uint64_t bit = 1ull << lane;
-      const uint64_t m[4] = {m0, m1, m2, m3};
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (m[s] & bit) {
-          if (p < kCandCap) c[p] = ((uint64_t)word_of(wv, s) << 32) | (4 * q + s);
-          ++p;
-        }
-      cnt += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-    }
+    cnt = filter_groups(ph, 0, (d32 + 3) / 4, d32, (uint32_t)(ts.tau - 1), c);
     if (ts.step(cnt, fo, kCandCap, &fail)) {
       ok = true;
       break;

@@ -6,8 +6,11 @@ Filter: lane q of an iteration holds the four keys of positions 4q..4q+3;
 four ballots mark the keys below tau, and a candidate's list index is the
 running count plus the marked keys of lower lanes (all four words) plus the
 lane's own earlier words, so the list is in ascending j; it is cut at 320
-entries but counted in full. A block splits a row into four consecutive
-quarters of groups, one per wave, and concatenates the lists.
+entries but counted in full. In an iteration whose positions all exist, the
+marks are only taken if some lane's smallest key is below tau, and when no
+lane has two marked keys, a marked lane's entry is its smallest key at the
+running count plus the marked lanes below it. A block splits a row into four
+consecutive quarters of groups, one per wave, and concatenates the lists.
 
 Select: list entry i sits in slot i // 64 of lane i % 64. A bitwise search
 from tau's top bit finds T, the largest value with fewer than fanout keys
@@ -31,9 +34,13 @@ def lanes_below(mask, lane):
     return bin(mask & ((1 << lane) - 1)).count("1")
 
 
+PATHS = {"skip": 0, "one_per_lane": 0, "general": 0}  # iterations by the kernel's branch
+
+
 def filter_groups(keys, g0, g1, tau):
     d = len(keys)
     tm1 = tau - 1
+    gf = min(g1, d // 4)  # groups below gf have all four positions
     c, cnt = [None] * CAP, 0
     for q0 in range(g0, g1, WAVE):
         m = [0, 0, 0, 0]
@@ -43,6 +50,24 @@ def filter_groups(keys, g0, g1, tau):
                 j = 4 * q + s
                 if q < g1 and j < d and keys[j] <= tm1:
                     m[s] |= 1 << lane
+        whole = q0 + WAVE <= gf
+        if whole:
+            mins = [min(keys[4 * (q0 + lane):4 * (q0 + lane) + 4]) for lane in range(WAVE)]
+            if not any(mn <= tm1 for mn in mins):
+                PATHS["skip"] += 1
+                continue
+            anym = m[0] | m[1] | m[2] | m[3]
+            if sum(bin(ms).count("1") for ms in m) == bin(anym).count("1"):
+                PATHS["one_per_lane"] += 1
+                for lane in range(WAVE):
+                    if (anym >> lane) & 1:
+                        s = next(x for x in range(4) if (m[x] >> lane) & 1)
+                        p = cnt + lanes_below(anym, lane)
+                        if p < CAP:
+                            c[p] = (mins[lane] << 32) | (4 * (q0 + lane) + s)
+                cnt += bin(anym).count("1")
+                continue
+            PATHS["general"] += 1
         for lane in range(WAVE):
             q = q0 + lane
             p = cnt + sum(lanes_below(ms, lane) for ms in m)
@@ -146,3 +171,20 @@ def test_small_keys_and_full_range_tau():
         for fo in (1, 4, 7):
             for tau in acceptable_taus(keys, fo):
                 assert sample_row(keys, fo, tau) == reference(keys, fo), (fo, tau)
+
+
+def test_both_append_paths_taken():
+    # the tests above reach the one-per-lane append and the general one
+    rnd = random.Random(5)
+    before = dict(PATHS)
+    for d in (1000, 4096):
+        keys = [rnd.getrandbits(32) for _ in range(d)]
+        for tau in acceptable_taus(keys, 10)[::20]:
+            assert sample_row(keys, 10, tau) == reference(keys, 10)
+    pool = [rnd.getrandbits(32) for _ in range(4)]
+    keys = [rnd.choice(pool) for _ in range(600)]  # lanes with several keys below tau
+    for tau in acceptable_taus(keys, 5):
+        assert sample_row(keys, 5, tau) == reference(keys, 5)
+    assert PATHS["one_per_lane"] > before["one_per_lane"]
+    assert PATHS["general"] > before["general"]
+    assert PATHS["skip"] > before["skip"]
