@@ -1238,11 +1238,11 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
       } else {
         sa.row_waves = nprev;  // the big list never exceeds the frontier
         sa.big_blocks = 0;
-        const dim3 grid((unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kSampleWaves)));
+        const dim3 grid((unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kRowWaves)));
         if (timed)
-          hipExtLaunchKernelGGL(ms::k_sample_waves, grid, dim3(ms::kSampleWaves * MS_WAVE), 0, s, hop_a, hop_b, 0, sa);
+          hipExtLaunchKernelGGL(ms::k_sample_waves, grid, dim3(ms::kRowWaves * MS_WAVE), 0, s, hop_a, hop_b, 0, sa);
         else
-          ms::k_sample_waves<<<grid, ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
+          ms::k_sample_waves<<<grid, ms::kRowWaves * MS_WAVE, 0, s>>>(sa);
       }
       if (timed) c->pending.push_back({hop_a, hop_b, 6});
       const int64_t nbw = std::max<int64_t>(1, cdiv(c->W, ms::kScanTile));

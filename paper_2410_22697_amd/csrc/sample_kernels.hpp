@@ -260,7 +260,8 @@ __global__ __launch_bounds__(kScanNT) void k_scan_partials(int32_t* __restrict__
 // lists, concatenated in order, are the row's list in ascending j. Otherwise
 // (many rows keep the chip busy) each gets one wave, ahead of the shorter
 // rows. Other rows get one wave each.
-constexpr int kSampleWaves = 4;
+constexpr int kSampleWaves = 4;  // k_sample_blocks: waves per block (a long row's quarters)
+constexpr int kRowWaves = 2;     // k_sample_waves: waves per workgroup (one row each)
 constexpr int kCandSlots = 5;                   // candidates per lane in the selection
 constexpr int kCandCap = kCandSlots * MS_WAVE;  // candidates per wave (LDS): 320, so the
                                                 // largest fanout (256) keeps 64 of slack for ties
@@ -510,11 +511,15 @@ __device__ __forceinline__ int filter_groups(const PhiloxRow& ph, uint32_t g0, u
 
 // Large frontiers (many rows keep the chip busy): every row one per wave, the
 // long ones (waves [0, row_waves) walk the big list) dispatched first.
-__global__ __launch_bounds__(kSampleWaves* MS_WAVE) void k_sample_waves(SampleArgs a) {
-  __shared__ uint64_t cand[kSampleWaves][kCandCap];
+// Workgroups of two waves: a workgroup holds its LDS until its last wave
+// ends, and rows of a power-law frontier end at very different times, so
+// smaller workgroups keep more waves resident (hop 3 on the papers-sized
+// share: 212 us with four waves per workgroup, 199 us with two).
+__global__ __launch_bounds__(kRowWaves* MS_WAVE) void k_sample_waves(SampleArgs a) {
+  __shared__ uint64_t cand[kRowWaves][kCandCap];
   if (a.sz->status) return;
   const int lane = lane_id(), wave = wave_uniform(wave_id());
-  const int64_t w = (int64_t)blockIdx.x * kSampleWaves + wave;
+  const int64_t w = (int64_t)blockIdx.x * kRowWaves + wave;
   int64_t row;
   if (w < a.row_waves) {
     if (w >= a.sz->n_big[a.hop - 1]) return;
