@@ -45,19 +45,19 @@ class Workload:
 WORKLOADS = {
     # 10K-node power law, 4 partitions: small enough for brute-force checks.
     "cl10k": Workload("cl10k", 10_000, 2.1, 10.0, False, 4, 64, "f32", 10, 256,
-                      (25, 10), 25, 0.95, 8, 50),
+                      (25, 10), 25, 0.95, 8, 50, note="none (CPU-oracle scale)"),
     # arxiv-sized: 170K nodes, ~1.17M directed edges, 8 partitions.
     "cl170k": Workload("cl170k", 170_000, 2.2, 7.0, True, 8, 128, "f32", 50, 1024,
-                       (15, 10, 5), 25, 0.95, 16, 200),
+                       (15, 10, 5), 25, 0.95, 16, 200, note="arxiv (Table 2)"),
     # products-sized: 2.45M nodes, ~62M undirected edges, 16 partitions.
     "cl2m45": Workload("cl2m45", 2_450_000, 2.0, 50.0, False, 16, 100, "f32", 8, 2000,
-                       (15, 10, 5), 25, 0.95, 32, 7),
+                       (15, 10, 5), 25, 0.95, 32, 7, note="products (Table 2)"),
     # same graph, bf16 rows and a stress eviction setting.
     "cl2m45_bf16": Workload("cl2m45_bf16", 2_450_000, 2.0, 50.0, False, 16, 100, "bf16", 8, 4096,
-                            (20, 15, 10), 50, 0.8, 4, 3),
+                            (20, 15, 10), 50, 0.8, 4, 3, note="products (Table 2), stress eviction"),
     # papers-sized share: partition 0 of 64 of a 111M-node, ~1.6B-edge graph.
     "cl111m_p64": Workload("cl111m_p64", 111_000_000, 1.9, 29.0, False, 64, 128, "f32", 1, 1024,
-                           (15, 10, 5), 25, 0.95, 32, 17),
+                           (15, 10, 5), 25, 0.95, 32, 17, note="one of 64 partitions of papers (Table 2)"),
 }
 
 
