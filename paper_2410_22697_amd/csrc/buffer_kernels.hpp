@@ -90,6 +90,8 @@ struct ClassifyArgs {
   const int32_t* slot_round;  // round that last refilled each slot
   const int32_t* landed;      // round whose refill row has landed in each slot
   int32_t pend_round;         // refill of this round may still be in flight (-1: none)
+  const int32_t* seeds;       // the step's seeds (their frontier positions are taken back if invalid)
+  int32_t n0;
 };
 
 constexpr int kClsNT = 256;
@@ -114,7 +116,16 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   constexpr int NW = kClsNT / MS_WAVE;
   __shared__ int32_t wc[NW][3];          // per-wave counts: hbm list, host list, pending hits
   __shared__ unsigned long long base[2];
-  if (a.sz->status) return;
+  if (a.sz->status) {
+    // invalid seeds: every kernel of the step has skipped, and the frontier
+    // positions k_seed_init marked are taken back, so the step leaves no trace
+    if (a.sz->status & 3)
+      for (int64_t i = (int64_t)blockIdx.x * kClsNT + threadIdx.x; i < a.n0; i += (int64_t)gridDim.x * kClsNT) {
+        const int32_t v = a.seeds[i];
+        if (v >= 0 && v < a.L) a.pos_of[v] = -1;
+      }
+    return;
+  }
   const int64_t n = a.sz->n[a.K];
   const int lane = lane_id(), wave = wave_id();
   const int64_t tile = (int64_t)kClsNT * kClsItems;

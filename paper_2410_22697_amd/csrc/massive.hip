@@ -1306,12 +1306,13 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
     ca.slot_round = c->d_slot_round;
     ca.landed = c->d_landed;
     ca.pend_round = pend;
+    ca.seeds = seeds;
+    ca.n0 = n0;
     // the frontier's size is known on the device only: at most kClsBlocks
     // blocks stride over it (a frontier far below the bound leaves the blocks
     // past its end idle, not a long tail of dispatches)
     ms::k_classify<<<grid_for(nb[c->K], ms::kClsNT * ms::kClsItems, ms::kClsBlocks), ms::kClsNT, 0, s>>>(ca);
   }
-  if (n0 > 0) ms::k_seed_undo<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, c->d_pos_of, sz);
   CK(hipEventRecord(c->ev_cls_done[slot], s));
   // The gathers run on the side stream, so the main stream goes on to the
   // next step's sampling at once. HBM rows first, at full bandwidth: after the

@@ -95,16 +95,6 @@ __global__ void k_seed_init(const int32_t* __restrict__ seeds, int32_t n0, int32
   nodes[i] = v;
 }
 
-// Undo k_seed_init's pos_of marks if the seeds failed validation (then every
-// other kernel of the step skipped, and the step leaves no trace).
-__global__ void k_seed_undo(const int32_t* __restrict__ seeds, int32_t n0, int32_t L,
-                            int32_t* __restrict__ pos_of, const StepSizes* sz) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n0 || !(sz->status & 3)) return;
-  const int32_t v = seeds[i];
-  if (v >= 0 && v < L) pos_of[v] = -1;
-}
-
 // ------------------------------------------------------ per-row counts + scan
 // Block b < nbk: the rows of tile b get min(deg(F[i]), fo) positions; the
 // tile's exclusive prefix comes from the single-pass scan, and bptr[0..n]
