@@ -123,6 +123,7 @@ struct StepSizes {
   int64_t local, hits, misses;
   int64_t n_hbm, n_miss;  // lengths of the two gather lists
   int64_t n_big[8];       // rows longer than the big-row threshold, per hop
+  int64_t n_small[8];     // the other rows, when they are listed too (one-wave-per-row sampler)
   int64_t n_local_new[8]; // new frontier nodes below L (local), per hop
   int64_t n_pending;      // hits on slots still refilling (read over the host link)
   int32_t status;    // != 0: invalid seeds; later kernels of the step skip

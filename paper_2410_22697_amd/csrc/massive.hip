@@ -1200,9 +1200,11 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
       // the previous hop's relabel shares the launch
       const int64_t nrel = k > 1 ? (int64_t)grid_for(eb[k - 2], ms::kScanTile, 1024) : 0;
+      // a large frontier lists every row for the one-wave-per-row sampler
+      const bool by_waves = nprev > ms::kBlockRowsMax;
       ms::k_row_scan<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
           c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], sb.flags, epoch(),
-          sb.big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of);
+          sb.big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of, by_waves ? nprev : 0);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;
@@ -1227,7 +1229,7 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
       // dispatch can carry its own start/stop events (timing group 6).
       hipEvent_t hop_a = nullptr, hop_b = nullptr;
       const bool timed = k == c->K && c->kernel_pair(6, &hop_a, &hop_b);
-      if (nprev <= ms::kBlockRowsMax) {
+      if (!by_waves) {
         sa.row_waves = 0;
         sa.big_blocks = std::max<int64_t>(1, std::min<int64_t>(nprev, c->big_blocks));
         const dim3 grid((unsigned)(sa.big_blocks + std::max<int64_t>(1, cdiv(nprev, ms::kSampleWaves))));
@@ -1236,9 +1238,9 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
         else
           ms::k_sample_blocks<<<grid, ms::kSampleWaves * MS_WAVE, 0, s>>>(sa);
       } else {
-        sa.row_waves = nprev;  // the big list never exceeds the frontier
+        sa.row_waves = nprev;  // the row list (nprev entries at most) ends there
         sa.big_blocks = 0;
-        const dim3 grid((unsigned)std::max<int64_t>(1, cdiv(2 * nprev, ms::kRowWaves)));
+        const dim3 grid((unsigned)std::max<int64_t>(1, cdiv(nprev, ms::kRowWaves)));
         if (timed)
           hipExtLaunchKernelGGL(ms::k_sample_waves, grid, dim3(ms::kRowWaves * MS_WAVE), 0, s, hop_a, hop_b, 0, sa);
         else

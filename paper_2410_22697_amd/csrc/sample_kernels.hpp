@@ -98,8 +98,12 @@ __global__ void k_seed_init(const int32_t* __restrict__ seeds, int32_t n0, int32
 // ------------------------------------------------------ per-row counts + scan
 // Block b < nbk: the rows of tile b get min(deg(F[i]), fo) positions; the
 // tile's exclusive prefix comes from the single-pass scan, and bptr[0..n]
-// gets the offsets. Rows longer than big_min go to big_rows (one global atomic
-// per block). Every load of a thread is issued before the first is used.
+// gets the offsets. Rows longer than big_min go to the front of big_rows (one
+// global atomic per block). With small_end > 0 the other rows go to its back,
+// the r-th listed one at big_rows[small_end - 1 - r]: with n <= small_end
+// rows the two parts never meet, and the one-wave-per-row sampler then finds
+// a row for each of its first n waves. Every load of a thread is issued
+// before the first is used.
 // Blocks b >= nbk relabel the previous hop's sampled ids (rel_ids, if given):
 // that work depends on the same kernels and shares the launch.
 __device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t e, const int32_t* __restrict__ pos_of,
@@ -132,11 +136,11 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
                                                       int32_t fo, int32_t* __restrict__ bptr, uint64_t* flags,
                                                       uint32_t epoch, int32_t* __restrict__ big_rows,
                                                       int64_t big_min, int64_t nbk, int32_t* __restrict__ rel_ids,
-                                                      const int32_t* __restrict__ pos_of) {
+                                                      const int32_t* __restrict__ pos_of, int64_t small_end) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
-  __shared__ int32_t big_lds[kScanTile];
-  __shared__ int32_t big_n;
-  __shared__ unsigned long long big_base;
+  __shared__ int32_t big_lds[kScanTile];  // long rows from the front, the others from the back
+  __shared__ int32_t big_n, small_n;
+  __shared__ unsigned long long big_base, small_base;
   __shared__ uint32_t excl_lds;
   if (sz->status) return;
   if ((int64_t)blockIdx.x >= nbk) {
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
   }
   const int64_t n = sz->n[hop - 1];
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  if (threadIdx.x == 0) big_n = 0;
+  if (threadIdx.x == 0) big_n = small_n = 0;
   __syncthreads();
   int32_t c[kScanItems] = {};
   int32_t s = 0;
@@ -173,7 +177,10 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
         const int64_t d = hi[it] - lo[it];
         c[it] = d < fo ? (int32_t)d : fo;
         s += c[it];
-        if (d > big_min) big_lds[atomicAdd(&big_n, 1)] = (int32_t)i;
+        if (d > big_min)
+          big_lds[atomicAdd(&big_n, 1)] = (int32_t)i;
+        else if (small_end)
+          big_lds[kScanTile - 1 - atomicAdd(&small_n, 1)] = (int32_t)i;
       }
     }
   }
@@ -196,9 +203,12 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
     }
     if ((int64_t)blockIdx.x == nbk - 1) sz->e[hop - 1] = (int64_t)before + tot;
     big_base = big_n ? atomicAdd((unsigned long long*)&sz->n_big[hop - 1], (unsigned long long)big_n) : 0ull;
+    small_base = small_n ? atomicAdd((unsigned long long*)&sz->n_small[hop - 1], (unsigned long long)small_n) : 0ull;
   }
   __syncthreads();
   for (int j = threadIdx.x; j < big_n; j += kScanNT) big_rows[big_base + j] = big_lds[j];
+  for (int j = threadIdx.x; j < small_n; j += kScanNT)
+    big_rows[small_end - 1 - (int64_t)(small_base + j)] = big_lds[kScanTile - 1 - j];
 }
 
 // Exclusive scan of partials[0..nb) in place (one block). Writes the total
@@ -274,7 +284,7 @@ struct SampleArgs {
   double mu32;              // (fo + 3 sqrt(fo) + 3) * 2^32
   int64_t big_min;          // rows longer than this are listed in big_rows
   const int32_t* big_rows;  // appended by k_row_scan
-  int64_t row_waves;        // k_sample_waves: waves [0, row_waves) take the big list, the rest all rows
+  int64_t row_waves;        // k_sample_waves: small_end of k_row_scan (the other rows' list ends there)
   int64_t big_blocks;       // k_sample_blocks: blocks [0, big_blocks) walk the big list, one row per
                             // block; the rest take all other rows, one per wave
   const int32_t* pos_of;    // frontier position of an id, or -1
@@ -500,7 +510,8 @@ __device__ __forceinline__ int filter_groups(const PhiloxRow& ph, uint32_t g0, u
 }
 
 // Large frontiers (many rows keep the chip busy): every row one per wave, the
-// long ones (waves [0, row_waves) walk the big list) dispatched first.
+// long ones (waves [0, n_big), the front of the row list) dispatched first,
+// then the others (waves [n_big, n), its back); waves from n on find no row.
 // Workgroups of two waves: a workgroup holds its LDS until its last wave
 // ends, and rows of a power-law frontier end at very different times, so
 // smaller workgroups keep more waves resident (hop 3 on the papers-sized
@@ -510,19 +521,13 @@ __global__ __launch_bounds__(kRowWaves* MS_WAVE) void k_sample_waves(SampleArgs 
   if (a.sz->status) return;
   const int lane = lane_id(), wave = wave_uniform(wave_id());
   const int64_t w = (int64_t)blockIdx.x * kRowWaves + wave;
-  int64_t row;
-  if (w < a.row_waves) {
-    if (w >= a.sz->n_big[a.hop - 1]) return;
-    row = wave_uniform((int32_t)a.big_rows[w]);
-  } else {
-    row = w - a.row_waves;
-    if (row >= a.sz->n[a.hop - 1]) return;
-  }
+  const int64_t nbig = a.sz->n_big[a.hop - 1];
+  if (w >= a.sz->n[a.hop - 1]) return;
+  const int64_t row = wave_uniform((int32_t)a.big_rows[w < nbig ? w : a.row_waves - 1 - (w - nbig)]);
   // the row, its node and its extent are the same in every lane
   const int32_t v = wave_uniform(a.nodes[row]);
   const int64_t start = wave_uniform(a.csr_indptr[v]);
   const int64_t d = wave_uniform(a.csr_indptr[v + 1]) - start;
-  if (w >= a.row_waves && d > a.big_min) return;  // taken by a wave of the big list
   const int32_t fo = a.fo;
   int32_t* out = a.out + a.bptr[row];
   const int32_t* nb = a.csr_indices + start;
