@@ -271,7 +271,8 @@ struct massive_ctx {
   hipEvent_t ev_get() {
     if (ev_pool.empty()) {
       hipEvent_t e;
-      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      // timing only: no system-scope fence
+      if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
       return e;
     }
     hipEvent_t e = ev_pool.back();
@@ -519,7 +520,7 @@ void link_timing(massive_ctx* c, int timing, int g, hipEvent_t* a, hipEvent_t* b
     if (!c->lev_pool.empty()) {
       *e = c->lev_pool.back();
       c->lev_pool.pop_back();
-    } else if (hipEventCreate(e) != hipSuccess) {
+    } else if (hipEventCreateWithFlags(e, hipEventDisableSystemFence) != hipSuccess) {  // timing only
       *e = nullptr;
     }
   }
@@ -861,9 +862,16 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   }
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
-  for (int i = 0; i < kSlots; ++i)
-    for (hipEvent_t* e : {&c->ev_cls_done[i], &c->ev_hbm_done[i], &c->ev_batch_done[i], &c->ev_miss_done[i]})
-      CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
+  // Events that only order work between this device's streams (classify ->
+  // gathers, HBM gather -> refill and round, miss gather -> round) skip the
+  // system-scope fence: their kernels' writes are visible on the device
+  // without it. The batch's completion event keeps it: after it the host
+  // reads the step's sizes and the caller its outputs.
+  for (int i = 0; i < kSlots; ++i) {
+    for (hipEvent_t* e : {&c->ev_cls_done[i], &c->ev_hbm_done[i], &c->ev_miss_done[i]})
+      CK(hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventDisableSystemFence));
+    CK(hipEventCreateWithFlags(&c->ev_batch_done[i], hipEventDisableTiming));
+  }
   for (hipEvent_t* e : {&c->ev_round_done, &c->ev_refill_done})
     CK(hipEventCreateWithFlags(e, hipEventDisableTiming));
   if (c->staged()) {
