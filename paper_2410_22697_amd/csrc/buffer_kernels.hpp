@@ -328,18 +328,64 @@ __global__ __launch_bounds__(256) void k_gather_hbm(const int2* __restrict__ lis
   __builtin_amdgcn_s_setprio(3);
   gather_body<V, ONE, 4>(list, count, src, dst, rb, cpr, magic);
 }
+// The step's completion, done by the step's last kernel on the side stream:
+// the slots written through are stamped landed for round `round_id` (none if
+// round_id < 0), and one block derives the step's counts (local rows: the
+// seeds plus the new nodes below L of each hop; hits: the HBM list's buffer
+// rows plus the hits read over the host link; misses: the rest of the host
+// list), then copies the step's sizes and the eviction-round consistency flag
+// into the pinned host mailbox (device view), made visible to the host. Every
+// value it copies is final once classify has run (the round it checks ran
+// before classify), and the host reads the mailbox only after the kernel ends.
+constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
+static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
+struct StepTail {
+  StepSizes* sz;
+  int32_t K;
+  const int32_t* bad;
+  StepSizes* h_sz;
+  int32_t* h_bad;
+  int32_t* landed;
+  int64_t cap;
+  int32_t round_id;
+};
+
+// one whole block of at least kSizeWords + 1 threads
+__device__ __forceinline__ void publish_step(const StepTail& t) {
+  const int i = threadIdx.x;
+  StepSizes* sz = t.sz;
+  if (i == 0 && !sz->status) {
+    int64_t local = sz->n[0];
+    for (int k = 0; k < t.K; ++k) local += sz->n_local_new[k];
+    sz->local = local;
+    sz->hits = sz->n_hbm - local + sz->n_pending;
+    sz->misses = sz->n_miss - sz->n_pending;
+  }
+  __syncthreads();
+  if (i < kSizeWords) reinterpret_cast<int32_t*>(t.h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
+  if (i == kSizeWords) *t.h_bad = *t.bad;
+  __threadfence_system();
+}
+
 // misses: pinned host store (over the host link) -> output rows. The list
 // also holds the hits on slots whose refill had not landed when the step was
 // classified; such a row is written into its buffer slot too (wslot >= 0), so
 // a replacement row crosses the link once, together with the misses (the
-// merged fetch of Algorithm 2). k_step_done then marks those slots landed.
+// merged fetch of Algorithm 2), and the lane that writes its first chunk
+// stamps the slot landed. Every kernel that reads a buffer row because of
+// that stamp (a later HBM gather) runs after this one in stream order; a
+// refill chunk that sees it skips a row this kernel writes anyway (same
+// bytes). Block 0 publishes the step (the completion above) once its share
+// of the rows is done, so no kernel follows this one in the step (publishing
+// first, beside the next step's sampling, measured 1.5% slower before the
+// first round).
 // dummy: a device row of row_bytes that lanes past the end move onto itself.
 template <typename V, bool ONE>
 __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int32_t* __restrict__ wslot,
                                                      const int64_t* __restrict__ count, const uint8_t* __restrict__ src,
                                                      uint8_t* __restrict__ dst, uint8_t* __restrict__ buf,
                                                      uint8_t* __restrict__ dummy, int64_t rb, uint32_t cpr,
-                                                     uint64_t magic) {
+                                                     uint64_t magic, StepTail tail) {
   constexpr int U = 4;
   const uint64_t n = (uint64_t)*count;
   const uint64_t total = n * cpr;
@@ -370,21 +416,21 @@ __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ li
     for (int u = 0; u < U; ++u) {
       uint8_t* q = in[u] ? dst + (uint64_t)(uint32_t)e[u].x * rb + off[u] : dummy + off[u];
       __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(q));
-      if (in[u] && ws[u] >= 0) *reinterpret_cast<V*>(buf + (uint64_t)(uint32_t)ws[u] * rb + off[u]) = v[u];
+      if (in[u] && ws[u] >= 0) {
+        *reinterpret_cast<V*>(buf + (uint64_t)(uint32_t)ws[u] * rb + off[u]) = v[u];
+        if (off[u] == 0 && tail.round_id >= 0 && ws[u] < tail.cap)
+          __hip_atomic_store(&tail.landed[ws[u]], tail.round_id, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
+  if (blockIdx.x == 0) publish_step(tail);
 }
 
-// The step's last kernel, after k_gather_miss (a kernel boundary: its row
-// writes are complete): the written-through slots are landed for round
-// `round_id` (none if round_id < 0), and block 0 derives the step's counts
-// (local rows: the seeds plus the new nodes below L of each hop; hits: the
-// HBM list's buffer rows plus the hits read over the host link; misses: the
-// rest of the host list), then copies the step's sizes and the eviction-round
-// consistency flag into the pinned host mailbox (device view), made visible
-// to the host before the kernel ends.
-constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
-static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
+// The step's completion as a kernel of its own, where no miss gather ends
+// the step (the staged host link, which scatters the host rows with other
+// kernels; a context without halo nodes): after the kernels that wrote the
+// step's rows (a kernel boundary), the written-through slots are stamped
+// landed, and block 0 publishes the step.
 __global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ wslot,
                                                    const int64_t* __restrict__ count, int32_t* __restrict__ landed,
                                                    int64_t cap, int32_t round_id, StepSizes* __restrict__ sz, int32_t K,
@@ -397,18 +443,8 @@ __global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ w
     }
   }
   if (blockIdx.x == 0) {
-    const int i = threadIdx.x;
-    if (i == 0 && !sz->status) {
-      int64_t local = sz->n[0];
-      for (int k = 0; k < K; ++k) local += sz->n_local_new[k];
-      sz->local = local;
-      sz->hits = sz->n_hbm - local + sz->n_pending;
-      sz->misses = sz->n_miss - sz->n_pending;
-    }
-    __syncthreads();
-    if (i < kSizeWords) reinterpret_cast<int32_t*>(h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
-    if (i == kSizeWords) *h_bad = *bad;
-    __threadfence_system();
+    const StepTail t{sz, K, bad, h_sz, h_bad, landed, cap, round_id};
+    publish_step(t);
   }
 }
 

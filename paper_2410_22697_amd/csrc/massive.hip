@@ -173,7 +173,6 @@ struct massive_ctx {
   // per step slot (step t uses slot t % MASSIVE_MAX_INFLIGHT): classify done
   // (main), HBM gather done and miss gather + mailbox done (side)
   hipEvent_t ev_cls_done[kSlots] = {}, ev_hbm_done[kSlots] = {}, ev_batch_done[kSlots] = {};
-  hipEvent_t ev_miss_done[kSlots] = {};  // the miss gather kernel (its write-through rows are in place)
   hipEvent_t ev_round_done = nullptr, ev_refill_done = nullptr;
   bool round_unclassified = false;  // a round was enqueued that no classify has waited for yet
   // The refill of the last round is copied in chunks, one after each of the
@@ -393,7 +392,8 @@ enum GatherKind { kHbm, kMiss };
 // rows (buf) of the hits on slots still refilling.
 void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, const int2* list,
                    const int64_t* count, const uint8_t* src, uint8_t* dst, int64_t rb, int64_t max_rows,
-                   int64_t max_blocks, const int32_t* wslot = nullptr, uint8_t* buf = nullptr) {
+                   int64_t max_blocks, const int32_t* wslot = nullptr, uint8_t* buf = nullptr,
+                   const ms::StepTail* tail = nullptr) {
   hipEvent_t ea = nullptr, eb = nullptr;
   const bool timed = c->kernel_pair(group, &ea, &eb);
   int vec = 4;
@@ -417,10 +417,10 @@ void launch_gather(massive_ctx* c, int group, GatherKind kind, hipStream_t s, co
     } else {                                                                                                   \
       if (timed)                                                                                               \
         hipExtLaunchKernelGGL(ms::k_gather_miss<V, ONE>, dim3(grid), dim3(256), 0, s, ea, eb, 0, list, wslot,  \
-                              count, src, dst, buf, c->d_dummy, rb, cpr, magic);                              \
+                              count, src, dst, buf, c->d_dummy, rb, cpr, magic, *tail);                       \
       else                                                                                                     \
         ms::k_gather_miss<V, ONE><<<grid, 256, 0, s>>>(list, wslot, count, src, dst, buf, c->d_dummy, rb, cpr, \
-                                                       magic);                                                 \
+                                                       magic, *tail);                                          \
     }                                                                                                          \
   } while (0)
 #define MS_KIND(V)          \
@@ -776,8 +776,7 @@ void free_ctx(massive_ctx* c) {
     if (p) (void)hipHostFree(p);
   if (c->d_ring) (void)hipFree(c->d_ring);
   for (int i = 0; i < kSlots; ++i)
-    for (hipEvent_t e : {c->ev_cls_done[i], c->ev_hbm_done[i], c->ev_batch_done[i], c->ev_miss_done[i],
-                         c->ev_rows_ready[i]})
+    for (hipEvent_t e : {c->ev_cls_done[i], c->ev_hbm_done[i], c->ev_batch_done[i], c->ev_rows_ready[i]})
       if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->ev_ring)
     if (e) (void)hipEventDestroy(e);
@@ -863,12 +862,12 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   CK(hipStreamCreateWithFlags(&c->s_miss, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
   // Events that only order work between this device's streams (classify ->
-  // gathers, HBM gather -> refill and round, miss gather -> round) skip the
-  // system-scope fence: their kernels' writes are visible on the device
-  // without it. The batch's completion event keeps it: after it the host
-  // reads the step's sizes and the caller its outputs.
+  // gathers, HBM gather -> refill and round) skip the system-scope fence:
+  // their kernels' writes are visible on the device without it. The batch's
+  // completion event keeps it: after it the host reads the step's sizes and
+  // the caller its outputs (the next round also follows it).
   for (int i = 0; i < kSlots; ++i) {
-    for (hipEvent_t* e : {&c->ev_cls_done[i], &c->ev_hbm_done[i], &c->ev_miss_done[i]})
+    for (hipEvent_t* e : {&c->ev_cls_done[i], &c->ev_hbm_done[i]})
       CK(hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventDisableSystemFence));
     CK(hipEventCreateWithFlags(&c->ev_batch_done[i], hipEventDisableTiming));
   }
@@ -1037,7 +1036,6 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
     CK(hipEventRecord(c->ev_cls_done[i], s));
     CK(hipEventRecord(c->ev_hbm_done[i], c->s_miss));
     CK(hipEventRecord(c->ev_batch_done[i], c->s_miss));
-    CK(hipEventRecord(c->ev_miss_done[i], c->s_miss));
   }
   CK(hipGetLastError());
   CK(hipStreamSynchronize(s));
@@ -1369,19 +1367,18 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
     int rc = launch_refill_chunks(c, 1, c->ev_hbm_done[slot]);
     if (rc != MASSIVE_OK) return rc;
   }
-  if (c->H > 0) {
+  // the miss gather ends the step: it stamps the slots it writes through as
+  // landed and publishes the step's sizes to the host mailbox (a context
+  // without halo nodes publishes them with a kernel of its own)
+  const ms::StepTail tail{sz, c->K, &c->d_ctr->bad, c->hd_sz + slot, c->hd_bad + slot, c->d_landed, c->cap,
+                          pend};
+  if (c->H > 0)
     launch_gather(c, 3, kMiss, sm, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
-                  c->host_blocks, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb);
-  }
-  CK(hipEventRecord(c->ev_miss_done[slot], sm));
-  // rows written through into their slots are landed from here on; the
-  // step's sizes go to the host mailbox
-  {
-    const bool publish = pend >= 0 && c->H > 0;
-    ms::k_step_done<<<publish ? grid_for(nb[c->K], 256, 1024) : 1, 256, 0, sm>>>(
-        sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, publish ? pend : -1, sz, c->K, &c->d_ctr->bad,
-        c->hd_sz + slot, c->hd_bad + slot);
-  }
+                  c->host_blocks, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb, &tail);
+  else
+    ms::k_step_done<<<1, 256, 0, sm>>>(sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, -1, sz, c->K,
+                                       &c->d_ctr->bad, c->hd_sz + slot, c->hd_bad + slot);
+  // (also the miss gather's completion, which the next round's refill follows)
   CK(hipEventRecord(c->ev_batch_done[slot], sm));
   CK(hipGetLastError());
   c->infl[slot].io = io;
@@ -1634,7 +1631,7 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
   // replacements into slots this round reassigns, so the new refill comes after
   // it (in the staged mode the link stream orders them: the worker enqueues
   // the new chunks after that step's tail)
-  if (!c->staged()) CK(hipStreamWaitEvent(s, c->ev_miss_done[tl % kSlots], 0));
+  if (!c->staged()) CK(hipStreamWaitEvent(s, c->ev_batch_done[tl % kSlots], 0));
   c->chunks_left = c->refill_chunks;
   c->round_pending_rows = true;
   CK(hipGetLastError());
