@@ -89,6 +89,10 @@ hipError_t scratch_address(int dev, void** out) {
 }  // namespace
 
 constexpr int kSlots = MASSIVE_MAX_INFLIGHT;
+// host-row bytes of a step above which its miss gather takes the larger grid
+// (at ~50 GB/s, ~0.5 ms of link time: about a sampling pass of the largest
+// workloads)
+constexpr int64_t kLinkHeavyBytes = 24ll << 20;
 constexpr int kTimingGroups = 7;  // bits of MASSIVE_TIMING_ALL
 
 struct massive_ctx {
@@ -108,7 +112,14 @@ struct massive_ctx {
   int64_t pmax = 0;     // partials capacity
   int64_t sort_cap = 0; // radix sort capacity
   int64_t hbm_blocks = 4096;  // grid bound of the HBM gather
-  int64_t host_blocks = 16;   // grid of the miss gather (host link)
+  // Grid of the miss gather (host link). Its reads hold memory-system
+  // resources for the whole link latency and slow the sampling beside them,
+  // so a step whose host-link work is light takes the smaller grid; a step
+  // that may be bound by the link (a refill in flight, or many host rows in
+  // the last step waited for) takes the larger one.
+  int64_t host_blocks = 16;
+  int64_t host_blocks_light = 12;
+  int64_t host_rows_seen = -1;  // host rows of the last step waited for (-1: none yet)
   int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
   int32_t* d_big = nullptr;             // big-row list of the current hop
@@ -839,7 +850,7 @@ int init_impl(massive_ctx* c, const massive_init_args* a) {
   }
 
   if (const char* e = getenv("MASSIVE_HBM_BLOCKS")) c->hbm_blocks = std::max(1, atoi(e));
-  if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = std::max(1, atoi(e));
+  if (const char* e = getenv("MASSIVE_HOST_BLOCKS")) c->host_blocks = c->host_blocks_light = std::max(1, atoi(e));
   if (const char* e = getenv("MASSIVE_REFILL_BLOCKS")) c->refill_blocks = std::max(1, atoi(e));
   // one chunk after each of the next steps' HBM gathers, all launched before
   // the step of the next round, so that round never waits for a chunk in flight
@@ -1372,9 +1383,12 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   // without halo nodes publishes them with a kernel of its own)
   const ms::StepTail tail{sz, c->K, &c->d_ctr->bad, c->hd_sz + slot, c->hd_bad + slot, c->d_landed, c->cap,
                           pend};
-  if (c->H > 0)
+  if (c->H > 0) {
+    const bool heavy = c->round_pending_rows || c->host_rows_seen < 0 || c->host_rows_seen * c->rb > kLinkHeavyBytes;
     launch_gather(c, 3, kMiss, sm, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
-                  c->host_blocks, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb, &tail);
+                  heavy ? c->host_blocks : c->host_blocks_light, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb,
+                  &tail);
+  }
   else
     ms::k_step_done<<<1, 256, 0, sm>>>(sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, -1, sz, c->K,
                                        &c->d_ctr->bad, c->hd_sz + slot, c->hd_bad + slot);
@@ -1471,6 +1485,7 @@ int massive_batch_wait(massive_ctx* c, massive_batch* io) {
   io->hits = z.hits;
   io->misses = z.misses;
   io->host_rows = z.n_miss;
+  c->host_rows_seen = z.n_miss;
   return MASSIVE_OK;
 }
 
