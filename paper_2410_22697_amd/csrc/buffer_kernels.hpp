@@ -377,7 +377,7 @@ __device__ __forceinline__ void publish_step(const StepTail& t) {
 // refill chunk that sees it skips a row this kernel writes anyway (same
 // bytes). Block 0 publishes the step (the completion above) once its share
 // of the rows is done, so no kernel follows this one in the step (publishing
-// first, beside the next step's sampling, measured 1.5% slower before the
+// first, beside the next step's sampling, measured ~2% slower before the
 // first round).
 // dummy: a device row of row_bytes that lanes past the end move onto itself.
 template <typename V, bool ONE>

@@ -81,7 +81,7 @@ def test_every_row_lands_once_in_its_list(n):
         assert sorted(hbm) == [i for i in range(n) if cls[i] in (0, 1)]
         assert sorted(host) == [i for i in range(n) if cls[i] >= 2]
         assert counters == [sum(c in (0, 1) for c in cls), sum(c >= 2 for c in cls)]
-        # the completion kernel's counts: local rows come from the dedup scans,
+        # the step's completion derives the counts: local rows come from the dedup scans,
         # pending hits from their own counter; hits and misses from the lists
         local, pending = sum(c == 0 for c in cls), sum(c == 3 for c in cls)
         hits, misses = counters[0] - local + pending, counters[1] - pending
