@@ -1,7 +1,8 @@
 """GPU parity at the edges of the argument ranges: one hop and the maximum of
 eight, fanouts at the top of their range (where the sampler's candidate list
-is nearly full), a partition without halo nodes, and a CSR with more than
-2^31 entries (64-bit row offsets past the 32-bit range)."""
+is nearly full), a partition without halo nodes, a CSR with more than 2^31
+entries (64-bit row offsets past the 32-bit range), long rows by few blocks,
+and host-link kernels at grids that do not divide their work."""
 import time
 
 import numpy as np
@@ -135,6 +136,20 @@ def test_long_rows_by_blocks(monkeypatch, big_row, big_blocks):
     assert rounds == 2
     prob, sched, w = workload_problem("cl10k", fanout=(200, 30), delta=3)
     run_parity("cl10k fanout 200 big rows > %d" % big_row, prob, sched.seeds, 6)
+
+
+@pytest.mark.parametrize("host_blocks,refill_blocks", [(1, 1), (5, 3)])
+def test_host_link_grids(monkeypatch, host_blocks, refill_blocks):
+    # the host-link kernels at grids that do not divide their work: with one
+    # block the miss gather's block 0 moves every row, stamps every
+    # written-through slot and then publishes the step; refills in flight on
+    # every step (a round every second step)
+    monkeypatch.setenv("MASSIVE_HOST_BLOCKS", str(host_blocks))
+    monkeypatch.setenv("MASSIVE_REFILL_BLOCKS", str(refill_blocks))
+    prob, sched, w = workload_problem("cl170k", delta=2)
+    rounds, hits, misses = run_parity("cl170k host grid %d, refill grid %d" % (host_blocks, refill_blocks), prob,
+                                      sched.seeds, 7, state_every=2, buffer_rows_every=2)
+    assert rounds == 3 and misses > 0
 
 
 def test_timing_groups():
