@@ -55,7 +55,7 @@ inline unsigned grid_for(int64_t n, int nt, int64_t cap = 16384) {
 
 // ------------------------------------------------------------- no-alloc path
 // massive_sample_noalloc takes a step's per-step buffers (sizes, the two
-// gather lists, the write-through slots, the big-row list, the scan flags)
+// gather lists, the write-through slots, the sampler's row list, the scan flags)
 // from this file-scope array instead of the context's. Layout: StepSizes
 // (512 B) | hbm list int2[kNoAllocMaxRows] | miss list int2[..] | write-through
 // slots int32[..] | big rows int32[..] | scan flags uint64[kNoAllocFlagWords].
@@ -122,7 +122,7 @@ struct massive_ctx {
   int64_t host_rows_seen = -1;  // host rows of the last step waited for (-1: none yet)
   int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
-  int32_t* d_big = nullptr;             // big-row list of the current hop
+  int32_t* d_big = nullptr;             // row list of the current hop (long rows first)
   int64_t big_min = ms::kBigRow;        // rows longer than this are sampled by a whole block
   int64_t big_blocks = ms::kBigBlocks;  // blocks that walk the list of such rows
   int32_t tau_iters = ms::kTauIters;    // threshold passes per row (0 makes every long row fail)
