@@ -348,6 +348,7 @@ struct StepTail {
   int32_t* landed;
   int64_t cap;
   int32_t round_id;
+  int32_t clear;  // the miss gather's last block clears the sizes after publishing them
 };
 
 // one whole block of at least kSizeWords + 1 threads
@@ -378,7 +379,9 @@ __device__ __forceinline__ void publish_step(const StepTail& t) {
 // bytes). Block 0 publishes the step (the completion above) once its share
 // of the rows is done, so no kernel follows this one in the step (publishing
 // first, beside the next step's sampling, measured ~2% slower before the
-// first round).
+// first round; publishing from the last block to finish, ~1% slower in the
+// link-bound steps). The last block to finish then clears the step's sizes,
+// so the slot's next step needs no clearing of its own (tail.clear).
 // dummy: a device row of row_bytes that lanes past the end move onto itself.
 template <typename V, bool ONE>
 __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ list, const int32_t* __restrict__ wslot,
@@ -424,6 +427,19 @@ __global__ __launch_bounds__(256) void k_gather_miss(const int2* __restrict__ li
     }
   }
   if (blockIdx.x == 0) publish_step(tail);
+  // the last block to finish clears the sizes for the slot's next step (every
+  // block has read its count, and block 0 has published them, by then)
+  __shared__ int last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    last = atomicAdd(&tail.sz->blocks_done, 1) == (int)gridDim.x - 1;
+  }
+  __syncthreads();
+  if (last && tail.clear) {
+    __threadfence();
+    for (int i = threadIdx.x; i < kSizeWords; i += blockDim.x) reinterpret_cast<int32_t*>(tail.sz)[i] = 0;
+  }
 }
 
 // The step's completion as a kernel of its own, where no miss gather ends
@@ -443,7 +459,7 @@ __global__ __launch_bounds__(256) void k_step_done(const int32_t* __restrict__ w
     }
   }
   if (blockIdx.x == 0) {
-    const StepTail t{sz, K, bad, h_sz, h_bad, landed, cap, round_id};
+    const StepTail t{sz, K, bad, h_sz, h_bad, landed, cap, round_id, 0};
     publish_step(t);
   }
 }

@@ -127,7 +127,7 @@ struct StepSizes {
   int64_t n_local_new[8]; // new frontier nodes below L (local), per hop
   int64_t n_pending;      // hits on slots still refilling (read over the host link)
   int32_t status;    // != 0: invalid seeds; later kernels of the step skip
-  int32_t pad;
+  int32_t blocks_done;  // blocks of the step's miss gather that have finished
 };
 
 // Eviction-round device scalars.

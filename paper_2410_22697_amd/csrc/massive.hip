@@ -120,6 +120,7 @@ struct massive_ctx {
   int64_t host_blocks = 16;
   int64_t host_blocks_light = 12;
   int64_t host_rows_seen = -1;  // host rows of the last step waited for (-1: none yet)
+  bool slot_clear[MASSIVE_MAX_INFLIGHT] = {};  // the slot's sizes were cleared by its last step's miss gather
   int64_t refill_blocks = 16; // grid of the refill (host link, off the critical path)
   double mu32[MASSIVE_MAX_HOPS] = {};    // sampler threshold targets, x 2^32
   int32_t* d_big = nullptr;             // row list of the current hop (long rows first)
@@ -1205,9 +1206,13 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
     ms::k_fill<int32_t><<<1, 256, 0, s>>>(reinterpret_cast<int32_t*>(sz), (int64_t)(sizeof(ms::StepSizes) / 4), 0);
     const int64_t words = std::max(cdiv(nb[c->K], ms::kScanTile), cdiv(c->W, ms::kScanTile)) + 1;
     ms::k_fill<uint64_t><<<grid_for(words, 256, 64), 256, 0, s>>>(sb.flags, words, 0ull);
-  } else {
+  } else if (!c->slot_clear[slot]) {
+    // (a slot's sizes are cleared by the miss gather of the step that last
+    // used it; the staged link and a context without halo nodes end a step
+    // with k_step_done, which does not clear them)
     CK(hipMemsetAsync(sz, 0, sizeof(ms::StepSizes), s));
   }
+  if (!sb.from_scratch) c->slot_clear[slot] = false;
   {
     massive_ctx::Range tr(c, s, 0);
     if (n0 > 0)
@@ -1382,12 +1387,13 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   // landed and publishes the step's sizes to the host mailbox (a context
   // without halo nodes publishes them with a kernel of its own)
   const ms::StepTail tail{sz, c->K, &c->d_ctr->bad, c->hd_sz + slot, c->hd_bad + slot, c->d_landed, c->cap,
-                          pend};
+                          pend, 1};
   if (c->H > 0) {
     const bool heavy = c->round_pending_rows || c->host_rows_seen < 0 || c->host_rows_seen * c->rb > kLinkHeavyBytes;
     launch_gather(c, 3, kMiss, sm, miss_list, &sz->n_miss, c->d_store, (uint8_t*)io->feat, c->rb, nb[c->K],
                   heavy ? c->host_blocks : c->host_blocks_light, sb.miss_slot, c->d_slab + (int64_t)c->L * c->rb,
                   &tail);
+    if (!sb.from_scratch) c->slot_clear[slot] = true;
   }
   else
     ms::k_step_done<<<1, 256, 0, sm>>>(sb.miss_slot, &sz->n_miss, c->d_landed, c->cap, -1, sz, c->K,
