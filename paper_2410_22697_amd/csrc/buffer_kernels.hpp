@@ -267,6 +267,46 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   }
 }
 
+// The step's completion, done by the step's last kernel on the side stream:
+// the slots written through are stamped landed for round `round_id` (none if
+// round_id < 0), and one block derives the step's counts (local rows: the
+// seeds plus the new nodes below L of each hop; hits: the HBM list's buffer
+// rows plus the hits read over the host link; misses: the rest of the host
+// list), then copies the step's sizes and the eviction-round consistency flag
+// into the pinned host mailbox (device view), made visible to the host. Every
+// value it copies is final once classify has run (the round it checks ran
+// before classify), and the host reads the mailbox only after the kernel ends.
+constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
+static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
+struct StepTail {
+  StepSizes* sz;
+  int32_t K;
+  const int32_t* bad;
+  StepSizes* h_sz;
+  int32_t* h_bad;
+  int32_t* landed;
+  int64_t cap;
+  int32_t round_id;
+  int32_t clear;  // the miss gather's last block clears the sizes (block 0 has published them by then)
+};
+
+// one whole block of at least kSizeWords + 1 threads
+__device__ __forceinline__ void publish_step(const StepTail& t) {
+  const int i = threadIdx.x;
+  StepSizes* sz = t.sz;
+  if (i == 0 && !sz->status) {
+    int64_t local = sz->n[0];
+    for (int k = 0; k < t.K; ++k) local += sz->n_local_new[k];
+    sz->local = local;
+    sz->hits = sz->n_hbm - local + sz->n_pending;
+    sz->misses = sz->n_miss - sz->n_pending;
+  }
+  __syncthreads();
+  if (i < kSizeWords) reinterpret_cast<int32_t*>(t.h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
+  if (i == kSizeWords) *t.h_bad = *t.bad;
+  __threadfence_system();
+}
+
 // ---------------------------------------------------------------- gather
 // dst row list[x].x <- src row list[x].y, as a bit copy of row_bytes. The
 // (row, chunk) work is flattened so every lane moves one vector per chunk
@@ -328,46 +368,6 @@ __global__ __launch_bounds__(256) void k_gather_hbm(const int2* __restrict__ lis
   __builtin_amdgcn_s_setprio(3);
   gather_body<V, ONE, 4>(list, count, src, dst, rb, cpr, magic);
 }
-// The step's completion, done by the step's last kernel on the side stream:
-// the slots written through are stamped landed for round `round_id` (none if
-// round_id < 0), and one block derives the step's counts (local rows: the
-// seeds plus the new nodes below L of each hop; hits: the HBM list's buffer
-// rows plus the hits read over the host link; misses: the rest of the host
-// list), then copies the step's sizes and the eviction-round consistency flag
-// into the pinned host mailbox (device view), made visible to the host. Every
-// value it copies is final once classify has run (the round it checks ran
-// before classify), and the host reads the mailbox only after the kernel ends.
-constexpr int kSizeWords = (int)(sizeof(StepSizes) / 4);
-static_assert(sizeof(StepSizes) % 4 == 0 && kSizeWords < 256, "mailbox copy: one word per thread");
-struct StepTail {
-  StepSizes* sz;
-  int32_t K;
-  const int32_t* bad;
-  StepSizes* h_sz;
-  int32_t* h_bad;
-  int32_t* landed;
-  int64_t cap;
-  int32_t round_id;
-  int32_t clear;  // the miss gather's last block clears the sizes after publishing them
-};
-
-// one whole block of at least kSizeWords + 1 threads
-__device__ __forceinline__ void publish_step(const StepTail& t) {
-  const int i = threadIdx.x;
-  StepSizes* sz = t.sz;
-  if (i == 0 && !sz->status) {
-    int64_t local = sz->n[0];
-    for (int k = 0; k < t.K; ++k) local += sz->n_local_new[k];
-    sz->local = local;
-    sz->hits = sz->n_hbm - local + sz->n_pending;
-    sz->misses = sz->n_miss - sz->n_pending;
-  }
-  __syncthreads();
-  if (i < kSizeWords) reinterpret_cast<int32_t*>(t.h_sz)[i] = reinterpret_cast<const int32_t*>(sz)[i];
-  if (i == kSizeWords) *t.h_bad = *t.bad;
-  __threadfence_system();
-}
-
 // misses: pinned host store (over the host link) -> output rows. The list
 // also holds the hits on slots whose refill had not landed when the step was
 // classified; such a row is written into its buffer slot too (wslot >= 0), so
