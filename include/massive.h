@@ -58,7 +58,8 @@ extern "C" {
 #define MASSIVE_EINVAL (-1)    /* bad argument (message in massive_last_error) */
 #define MASSIVE_ECAPACITY (-2) /* an output buffer is smaller than the bound  */
 #define MASSIVE_ENOMEM (-3)    /* device or host allocation failed            */
-#define MASSIVE_EHIP (-4)      /* HIP runtime error                           */
+#define MASSIVE_EHIP (-4)      /* HIP runtime error; from a step or a round, the
+                                  context then takes no further work         */
 #define MASSIVE_ESTATE (-5)    /* call out of order (see massive_sample)      */
 
 #define MASSIVE_MAX_HOPS 8

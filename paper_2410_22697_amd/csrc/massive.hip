@@ -1424,7 +1424,11 @@ int massive_sample_async(massive_ctx* c, const int32_t* seeds, int32_t n0, massi
     return c->fail(MASSIVE_ESTATE, "%d batches in flight: wait for the oldest one first", kSlots);
   const StepBufs sb{c->d_sz + slot, c->d_hbm_list[slot], c->d_miss_list[slot], c->d_miss_slot[slot], c->d_big,
                     c->d_scan_flags, false};
-  return enqueue_step(c, seeds, n0, io, nb, eb, sb);
+  rc = enqueue_step(c, seeds, n0, io, nb, eb, sb);
+  // a HIP call that failed part-way left work on the queues that no batch
+  // tracks: the context takes no further work
+  if (rc == MASSIVE_EHIP) c->broken = true;
+  return rc;
 }
 
 int massive_batch_wait(massive_ctx* c, massive_batch* io) {
@@ -1531,12 +1535,16 @@ int massive_sample_noalloc(massive_ctx* c, const int32_t* seeds, int32_t n0, mas
   c->timing = 0;
   rc = enqueue_step(c, seeds, n0, io, nb, eb, sb);
   c->timing = timing;
+  if (rc == MASSIVE_EHIP) c->broken = true;  // as in massive_sample_async
   if (rc != MASSIVE_OK) return rc;
   return massive_batch_wait(c, io);
 }
 
-int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t* replaced, int64_t* k_out) {
-  if (!c) return MASSIVE_EINVAL;
+}  // extern "C"
+
+namespace {
+
+int evict_step_impl(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t* replaced, int64_t* k_out) {
   if (c->broken) return c->fail(MASSIVE_ESTATE, "context is unusable after an earlier failure");
   if (!c->pending_round) return c->fail(MASSIVE_ESTATE, "no sampled step owes an eviction round");
   if (k_out) *k_out = 0;
@@ -1665,6 +1673,19 @@ int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t
     *k_out = c->h_rs->k;
   }
   return MASSIVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int massive_evict_step(massive_ctx* c, int32_t* evicted, int32_t* slots, int32_t* replaced, int64_t* k_out) {
+  if (!c) return MASSIVE_EINVAL;
+  const int rc = evict_step_impl(c, evicted, slots, replaced, k_out);
+  // a round that failed part-way on a HIP call leaves the buffer state
+  // undefined: the context takes no further work
+  if (rc == MASSIVE_EHIP) c->broken = true;
+  return rc;
 }
 
 int massive_get_counters(massive_ctx* c, int64_t* rounds, int64_t* evicted, int64_t* refilled) {
