@@ -118,7 +118,7 @@ __global__ __launch_bounds__(kClsNT) void k_classify(ClassifyArgs a) {
   __shared__ unsigned long long base[2];
   if (a.sz->status) {
     // invalid seeds: every kernel of the step has skipped, and the frontier
-    // positions k_seed_init marked are taken back, so the step leaves no trace
+    // positions the seed check marked are taken back, so the step leaves no trace
     if (a.sz->status & 3)
       for (int64_t i = (int64_t)blockIdx.x * kClsNT + threadIdx.x; i < a.n0; i += (int64_t)gridDim.x * kClsNT) {
         const int32_t v = a.seeds[i];

@@ -1215,8 +1215,6 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
   if (!sb.from_scratch) c->slot_clear[slot] = false;
   {
     massive_ctx::Range tr(c, s, 0);
-    if (n0 > 0)
-      ms::k_seed_init<<<grid_for(n0, 256, 1 << 30), 256, 0, s>>>(seeds, n0, c->L, io->nodes, c->d_pos_of, sz);
     for (int k = 1; k <= c->K; ++k) {
       const int64_t nprev = nb[k - 1];
       const int64_t nbk = std::max<int64_t>(1, cdiv(nprev, ms::kScanTile));
@@ -1226,7 +1224,8 @@ int enqueue_step(massive_ctx* c, const int32_t* seeds, int32_t n0, massive_batch
       const bool by_waves = nprev > ms::kBlockRowsMax;
       ms::k_row_scan<<<(unsigned)(nbk + nrel), ms::kScanNT, 0, s>>>(
           c->d_indptr, io->nodes, sz, k, c->fo[k - 1], io->indptr[k - 1], sb.flags, epoch(),
-          sb.big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of, by_waves ? nprev : 0);
+          sb.big, c->big_min, nbk, k > 1 ? io->indices[k - 2] : nullptr, c->d_pos_of, by_waves ? nprev : 0,
+          k == 1 ? seeds : nullptr, n0, c->L);
       ms::SampleArgs sa;
       sa.csr_indptr = c->d_indptr;
       sa.csr_indices = c->d_indices;

@@ -76,25 +76,6 @@ __device__ __forceinline__ uint32_t lookback_exclusive(uint64_t* flags, int64_t 
   return *excl_lds;
 }
 
-// ---------------------------------------------------------------- seeds
-// F_0 = seeds; pos_of[seed] = its position. Flags out-of-range or repeated
-// seeds in sz->status (the step is then abandoned by every later kernel).
-__global__ void k_seed_init(const int32_t* __restrict__ seeds, int32_t n0, int32_t L,
-                            int32_t* __restrict__ nodes, int32_t* __restrict__ pos_of,
-                            StepSizes* sz) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) sz->n[0] = n0;
-  if (i >= n0) return;
-  const int32_t v = seeds[i];
-  if (v < 0 || v >= L) {
-    atomicOr(&sz->status, 1);
-    return;
-  }
-  const int32_t prev = atomicCAS(&pos_of[v], -1, i);
-  if (prev != -1) atomicOr(&sz->status, 2);
-  nodes[i] = v;
-}
-
 // ------------------------------------------------------ per-row counts + scan
 // Block b < nbk: the rows of tile b get min(deg(F[i]), fo) positions; the
 // tile's exclusive prefix comes from the single-pass scan, and bptr[0..n]
@@ -106,6 +87,10 @@ __global__ void k_seed_init(const int32_t* __restrict__ seeds, int32_t n0, int32
 // before the first is used.
 // Blocks b >= nbk relabel the previous hop's sampled ids (rel_ids, if given):
 // that work depends on the same kernels and shares the launch.
+// For hop 1 (seeds given) the rows are the seed batch: the launch also checks
+// each seed (a local id, not repeated: the first to mark pos_of keeps it) and
+// places it, F_0 = seeds, pos_of[seed] = its position, n_0 = n0; a bad seed
+// sets the step's status, which every later kernel checks first.
 __device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t e, const int32_t* __restrict__ pos_of,
                                               int64_t b, int64_t nblocks) {
   for (int64_t b0 = b * kScanTile; b0 < e; b0 += nblocks * kScanTile) {
@@ -132,11 +117,12 @@ __device__ __forceinline__ void relabel_tiles(int32_t* __restrict__ ids, int64_t
 }
 
 __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict__ csr_indptr,
-                                                      const int32_t* __restrict__ nodes, StepSizes* sz, int hop,
+                                                      int32_t* __restrict__ nodes, StepSizes* sz, int hop,
                                                       int32_t fo, int32_t* __restrict__ bptr, uint64_t* flags,
                                                       uint32_t epoch, int32_t* __restrict__ big_rows,
                                                       int64_t big_min, int64_t nbk, int32_t* __restrict__ rel_ids,
-                                                      const int32_t* __restrict__ pos_of, int64_t small_end) {
+                                                      int32_t* __restrict__ pos_of, int64_t small_end,
+                                                      const int32_t* __restrict__ seeds, int32_t n0, int32_t L) {
   __shared__ int32_t lds[kScanNT / MS_WAVE + 1];
   __shared__ int32_t big_lds[kScanTile];  // long rows from the front, the others from the back
   __shared__ int32_t big_n, small_n;
@@ -147,7 +133,11 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
     if (rel_ids) relabel_tiles(rel_ids, sz->e[hop - 2], pos_of, blockIdx.x - nbk, gridDim.x - nbk);
     return;
   }
-  const int64_t n = sz->n[hop - 1];
+  // hop 1 with seeds: the rows are the seeds, which this launch checks and
+  // places (F_0 = seeds, pos_of[seed] = its position; an out-of-range or
+  // repeated seed flags the step, which every later kernel then abandons)
+  const int64_t n = seeds ? (int64_t)n0 : sz->n[hop - 1];
+  if (seeds && blockIdx.x == 0 && threadIdx.x == 0) sz->n[0] = n0;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   if (threadIdx.x == 0) big_n = small_n = 0;
   __syncthreads();
@@ -157,9 +147,26 @@ __global__ __launch_bounds__(kScanNT) void k_row_scan(const int64_t* __restrict_
     int32_t v[kScanItems];
     int64_t lo[kScanItems], hi[kScanItems];
 #pragma unroll
-    for (int it = 0; it < kScanItems; ++it) v[it] = nodes[base + it < n ? base + it : n - 1];
+    for (int it = 0; it < kScanItems; ++it) v[it] = (seeds ? seeds : nodes)[base + it < n ? base + it : n - 1];
 #pragma unroll
     for (int it = 0; it < kScanItems; ++it) pin(v[it]);
+    if (seeds) {
+#pragma unroll
+      for (int it = 0; it < kScanItems; ++it) {
+        const int64_t i = base + it;
+        const int32_t x = v[it];
+        const bool ok = x >= 0 && x < L;
+        if (i < n) {
+          if (!ok) {
+            atomicOr(&sz->status, 1);
+          } else {
+            if (atomicCAS(&pos_of[x], -1, (int32_t)i) != -1) atomicOr(&sz->status, 2);
+            nodes[i] = x;
+          }
+        }
+        v[it] = ok ? x : 0;  // an in-range row for the loads below (the step is abandoned anyway)
+      }
+    }
 #pragma unroll
     for (int it = 0; it < kScanItems; ++it) {
       lo[it] = csr_indptr[v[it]];
