@@ -24,6 +24,8 @@ Prints one JSON line for the papers-sized share (cl111m_p64):
   - cpu_baseline: the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
+import contextlib
+import gc
 import json
 import os
 import sys
@@ -129,6 +131,21 @@ class SharedInputs:
         import shutil
         shutil.rmtree(self.dir, ignore_errors=True)
         return False
+
+
+@contextlib.contextmanager
+def no_gc():
+    """A timed region without Python's garbage collector: a full collection
+    first, none inside (one landing in a timed window cost ~37 ms after a long
+    earlier context in the same process)."""
+    gc.collect()
+    was = gc.isenabled()
+    gc.disable()
+    try:
+        yield
+    finally:
+        if was:
+            gc.enable()
 
 
 def window_plan(warmup, steps, delta, limit=20000):
@@ -253,10 +270,11 @@ def run_context(w, g, local, store, sched, windows, depth=None, log_steps=False,
         f0 = gm.refilled_rows()
         gm.set_timing(groups)
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        run(a, b)
-        torch.cuda.synchronize()
-        el = time.perf_counter() - t0
+        with no_gc():
+            t0 = time.perf_counter()
+            run(a, b)
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
         tim = gm.timing()
         r1, e1 = gm.counters()
         f1 = gm.refilled_rows()
@@ -478,14 +496,15 @@ def oracle_full_run(w, g, local, store, sched, n, res):
     import oracle
     orc = oracle.Oracle(g.L, g.H, g.indptr, g.indices, g.halo_gid, g.halo_degree, local, store.numpy(),
                         w.row_bytes, w.fanout, w.buffer_pct, w.gamma, w.delta, w.philox_seed)
-    t0 = time.perf_counter()
-    for t in range(n):
-        st = orc.sample(sched.seeds(t))
-        orc.evict_step()
-        (gn, ge), row = res["sizes"][t], res["stats"][t]
-        if gn != st.n or ge != st.e or (int(row[0]), int(row[1]), int(row[2])) != (st.local, st.hits, st.misses):
-            raise SystemExit("bench: %s step %d differs from the oracle" % (w.name, t))
-    el = time.perf_counter() - t0
+    with no_gc():
+        t0 = time.perf_counter()
+        for t in range(n):
+            st = orc.sample(sched.seeds(t))
+            orc.evict_step()
+            (gn, ge), row = res["sizes"][t], res["stats"][t]
+            if gn != st.n or ge != st.e or (int(row[0]), int(row[1]), int(row[2])) != (st.local, st.hits, st.misses):
+                raise SystemExit("bench: %s step %d differs from the oracle" % (w.name, t))
+        el = time.perf_counter() - t0
     return {"value": round(n / el, 3), "unit": "minibatches/s", "cores": 1, "kind": "oracle",
             "sample": "the whole %d-step run from init; every step's sizes and class counts equal the GPU's" % n}
 
@@ -1003,10 +1022,11 @@ def overlap(w, g, local, store, sched, args):
 
     def timed(fn, *a):
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        fn(*a)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / W
+        with no_gc():
+            t0 = time.perf_counter()
+            fn(*a)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) / W
 
     lookahead(8, None)
     gm.set_timing(True)
@@ -1021,11 +1041,12 @@ def overlap(w, g, local, store, sched, args):
         for _ in range(3):
             train(tr, slot, n)
         consumer.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(20):
-            train(tr, slot, n)
-        consumer.synchronize()
-        t_ddp = (time.perf_counter() - t0) / 20
+        with no_gc():
+            t0 = time.perf_counter()
+            for _ in range(20):
+                train(tr, slot, n)
+            consumer.synchronize()
+            t_ddp = (time.perf_counter() - t0) / 20
         serial(8, tr)
         T_ser = timed(serial, W, tr)
         lookahead(8, tr)
